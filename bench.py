@@ -1,0 +1,206 @@
+#!/usr/bin/env python3
+"""Benchmark of the DSDE verification step on one MI355X.
+
+One step = dsde_verify + dsde_kld_signal + dsde_next_sl over one batch of
+synthetic inputs already resident in HBM (workload b256 by default: B=256,
+SL ~ U{1..8}, V=128256 bf16, T = 0.7 / 1.0 alternating).  Two input copies
+alternate between steps so that no step finds its logits in the 256 MB
+last-level cache.
+
+Prints one JSON line: rows/s over all logit rows of the step (2N + B), the
+algorithmic HBM rate, the roofline of the dominant kernel (the row-statistics
+pass, timed with HIP events recorded by the library on the launch stream), and
+the CPU oracle timed on the host as a baseline.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "verified logit rows/sec + achieved HBM GB/s (V=128256 bf16, B=256)"
+PEAK_HBM_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="b256")
+    ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU time of the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="measured HBM traffic of the row-statistics kernel (from rocprofv3 counters)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain device copy of known size (for scaling the counters)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see the design notes on how the step would shard)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2509_01083_amd as dsde
+    import workloads as W
+
+    dsde.load()
+    dev = torch.device("cuda:0")
+    cfg = W.CONFIGS[args.workload]
+    sl = W.sample_sl(cfg, args.seed)
+    copies = [W.make_step(cfg, seed=args.seed + i, device=dev, sl=sl) for i in range(2)]
+    st = W.make_signal_state(cfg, seed=args.seed, device=dev)
+    s0 = copies[0]
+    B, N, V, k_max = s0.B, s0.N, s0.V, s0.k_max
+    esz = 2 if s0.target.dtype == torch.bfloat16 else 4
+    ws = dsde.new_workspace(B, N, V, k_max, device=dev)
+    outs = [None, None]
+    sig_out = None
+    nsl_out = None
+
+    def one_step(i):
+        nonlocal sig_out, nsl_out
+        s = copies[i % 2]
+        outs[i % 2] = dsde.verify(s.target, s.draft, s.sl, s.cu_sl, s.draft_tokens, s.temperature, s.u_acc,
+                                  s.u_res, k_max, out=outs[i % 2], workspace=ws)
+        sig_out = dsde.kld_signal(s.sl, s.cu_sl, outs[i % 2]["kld"], st.hist, st.head, st.count, out=sig_out)
+        nsl_out = dsde.next_sl(sig_out["sf"], sig_out["wvir"], st.sl_max, 2.0, k_max, out=nsl_out)
+
+    for i in range(args.warmup):
+        one_step(i)
+    torch.cuda.synchronize()
+
+    # per-step HIP events around the row-statistics kernel, recorded by the library
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    stream = torch.cuda.current_stream()
+    for a, b in ev:  # materialise the underlying events
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    step_ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    step_ev[0].record(stream)
+    for i in range(args.steps):
+        dsde.set_profile_events(*ev[i])
+        one_step(args.warmup + i)
+    step_ev[1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dsde.set_profile_events(None, None)
+
+    gpu_ms = step_ev[0].elapsed_time(step_ev[1])
+    ms_per_step = gpu_ms / args.steps
+    k1_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    rows = 2 * N + B
+    acc = outs[(args.warmup + args.steps - 1) % 2]["accepted"].cpu().numpy()
+    sls = s0.sl.cpu().numpy()
+    b_full = int((acc == sls).sum())
+    io_bytes = 4 * (3 * N + 2 * B + B * (k_max + 1)) + 8 * B * cfg["W"]
+    alg_bytes = (2 * N + b_full) * V * esz + io_bytes
+    k1_bytes = 2 * N * V * esz  # every drafted pair read once
+    k1_gbps = k1_bytes / (k1_ms * 1e-3) / 1e9
+
+    traffic = None
+    if os.path.exists(args.traffic):
+        with open(args.traffic) as f:
+            tr = json.load(f)
+        if tr.get("workload") == args.workload and tr.get("kernel_source_hash") == kernel_hash():
+            traffic = tr.get("bytes_per_launch")
+
+    result = {
+        "metric": METRIC,
+        "value": rows / (ms_per_step * 1e-3),
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if esz == 2 else "fp32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "B": B, "N": N, "V": V, "rows_per_step": rows, "k_max": k_max,
+                   "logit_bytes_per_step": rows * V * esz, "seed": args.seed},
+        "hbm_gbps_algorithmic": alg_bytes / (ms_per_step * 1e-3) / 1e9,
+        "hbm_frac_algorithmic": alg_bytes / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+        "wall_ms_per_step": wall * 1e3 / args.steps,
+        "b_full": b_full,
+        "roofline": {"bound": "hbm", "kernel": "pair_stats_kernel", "achieved": k1_gbps, "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": k1_gbps / PEAK_HBM_GBPS, "traffic": traffic,
+                     "kernel_ms": k1_ms, "algorithmic_bytes": k1_bytes},
+        "cpu_baseline": None,
+    }
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"], result["parity"] = cpu_baseline(copies[(args.warmup + args.steps - 1) % 2],
+                                                                outs[(args.warmup + args.steps - 1) % 2],
+                                                                args.cpu_seconds)
+    if args.copy_calibration:
+        n = 1 << 30
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = n
+    print(json.dumps(result), flush=True)
+
+
+def kernel_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("verify.hip", "common.hpp"):
+        with open(os.path.join(ROOT, "paper_2509_01083_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def cpu_baseline(step, out, seconds):
+    """The oracle, as it stands, on the host: whole steps repeated until about
+    ``seconds`` of CPU time have passed; also checks the GPU step against it."""
+    import numpy as np
+
+    import oracle
+    import workloads as W
+    host = W.host_arrays(step)
+    threads = min(16, os.cpu_count() or 1)
+    t0 = time.perf_counter()
+    n = 0
+    ref = None
+    while True:
+        ref = oracle.verify(**host, n_threads=threads)
+        n += 1
+        if time.perf_counter() - t0 >= seconds or n >= 20:
+            break
+    dt = (time.perf_counter() - t0) / n
+    rows = 2 * int(host["cu_sl"][-1]) + len(host["sl"])
+    # parity of the timed GPU step against the oracle (ties excluded)
+    acc = out["accepted"].cpu().numpy()
+    tok = out["tokens"].cpu().numpy()
+    ok = (ref["seq_err"] == 0) & (ref["acc_tie"] == 0) & (ref["cdf_tie"] == 0)
+    mism = int((ok & ((acc != ref["accepted"]) | (tok != ref["tokens"]).any(axis=1))).sum())
+    kg = out["kld"].cpu().numpy().astype(np.float64)
+    kerr = float(np.max(np.abs(kg - ref["kld"]) / np.maximum(np.abs(ref["kld"]), 1e-12)))
+    cpu = {"value": rows / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
+           "sample": f"the full timed step (B={len(host['sl'])}, {rows} logit rows, V={host['V']}), "
+                     f"{n} repetition(s), {threads} threads, fp64",
+           "seconds_per_step": dt}
+    parity = {"compared": int(ok.sum()), "ties": int((ref["acc_tie"] | ref["cdf_tie"]).sum()),
+              "mismatches": mism, "kld_max_rel_err": kerr}
+    return cpu, parity
+
+
+if __name__ == "__main__":
+    main()

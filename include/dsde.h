@@ -1,0 +1,186 @@
+/*
+ * dsde.h -- C ABI of the DSDE speculative-verification hot path on MI355X.
+ *
+ * DSDE (arXiv 2509.01083) verifies, in one batched step, a ragged set of
+ * drafted tokens: sequence b proposes SL_b tokens (its own speculation length,
+ * Sec. 3.2 "Ragged Q"); the target model scores SL_b + 1 positions and the draft
+ * model SL_b.  This library computes, from the two models' logits:
+ *   - for every drafted position, the tempered softmaxes p (target) and
+ *     q (draft) and the per-token KL(p || q) used by the SL adapter (Sec. 3.1.2);
+ *   - the speculative-sampling acceptance scan (accept while u < min(1, p/q)),
+ *     the draw from the normalised residual max(0, p - q) at the first
+ *     rejection, or the bonus token from the extra target row when every drafted
+ *     token is accepted (Secs. 2.1 and 3.2);
+ *   - the KLD stability signal: mu_KLD,last, the recency-weighted mean and
+ *     variance over a short and a long window, WVIR and SF (Eqs. 3-7);
+ *   - the next speculation length per sequence (Eqs. 2 and 8) under the batch
+ *     cap SL_cap = mean of the predicted lengths (Sec. 3.3, Eqs. 9-11).
+ *
+ * Conventions (every function):
+ *   - Every array pointer is a caller-owned DEVICE buffer (e.g. a tensor's data
+ *     pointer), contiguous, of the stated shape and type.  The library never
+ *     allocates, frees or synchronises on these paths; work is enqueued
+ *     asynchronously on `stream` (a hipStream_t; NULL means the null stream).
+ *   - Scratch space comes from a caller workspace sized by
+ *     dsde_verify_workspace_bytes.  Calls with distinct workspaces and outputs
+ *     may run concurrently on different streams.
+ *   - Host-side argument errors are detected before any HIP call and return
+ *     DSDE_INVALID_ARG or DSDE_WORKSPACE_TOO_SMALL; nothing is enqueued then.
+ *     DSDE_DEVICE_ERROR reports a failed kernel launch.
+ *   - Data errors found on the device are reported per sequence in seq_err[b]
+ *     (bits DSDE_ERR_*).  A flagged sequence gets defined outputs: accepted = 0,
+ *     every token = pad_id, kld = NaN at its positions (not written when the
+ *     layout itself is invalid), NaN signal values, and it is left out of the cap.
+ *
+ * Packed ragged layout (no padding rows): with N = sum_b SL_b and
+ * cu_sl[b] = SL_0 + ... + SL_{b-1} (cu_sl[0] = 0, cu_sl[B] = N),
+ *   drafted position (b, j), j < SL_b  ->  index cu_sl[b] + j      in [0, N)
+ *   its target row                      ->  cu_sl[b] + b + j        in [0, N+B)
+ *   the bonus row of b                  ->  cu_sl[b] + b + SL_b
+ *   its draft row                       ->  cu_sl[b] + j            in [0, N)
+ * Logits are row-major [rows, V], fp32 or bf16.
+ */
+#ifndef DSDE_H_
+#define DSDE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DSDE_ABI_VERSION 1
+
+/* status codes */
+#define DSDE_OK 0
+#define DSDE_INVALID_ARG 1
+#define DSDE_WORKSPACE_TOO_SMALL 2
+#define DSDE_DEVICE_ERROR 3
+
+/* logit element types */
+#define DSDE_FP32 0
+#define DSDE_BF16 1
+
+/* per-sequence device error bits */
+#define DSDE_ERR_LAYOUT 1u   /* SL_b outside [0, k_max], or cu_sl not the prefix sums of sl with cu_sl[B] = N */
+#define DSDE_ERR_TOKEN 2u    /* a drafted token outside [0, V) */
+#define DSDE_ERR_LOGIT 4u    /* NaN or +-inf in a row the step reads (every drafted pair; the bonus row
+                                only when it is sampled) */
+#define DSDE_ERR_TEMP 8u     /* temperature not finite or not > 0 */
+#define DSDE_ERR_UNIFORM 16u /* a uniform outside [0, 1) */
+#define DSDE_ERR_SIGNAL 32u  /* non-finite KLD, SF, WVIR or SL_max, or SL_max < sl_min */
+#define DSDE_ERR_STATE 64u   /* ring head outside [0, W) or count outside [0, W] */
+
+/* Largest supported speculation length bound (one wavefront lane per drafted position). */
+#define DSDE_MAX_K 63
+
+/* The ABI version this library implements (DSDE_ABI_VERSION). */
+int32_t dsde_abi_version(void);
+
+/* A static description of a status code; never NULL. */
+const char *dsde_status_string(int32_t status);
+
+/* Workspace bytes dsde_verify needs for B sequences, N drafted positions,
+ * vocabulary V and speculation bound k_max; 0 when the sizes are invalid. */
+size_t dsde_verify_workspace_bytes(int32_t B, int64_t N, int64_t V, int32_t k_max);
+
+/*
+ * One batched verification step (speculative sampling, Sec. 2.1; ragged
+ * per-sequence lengths and the bonus/pad handling of Sec. 3.2; per-token KLD of
+ * Sec. 3.1.2).
+ *
+ *   target_logits [N+B, V]  dtype       target rows in the packed layout above
+ *   draft_logits  [N, V]    dtype       draft rows (may be NULL when N = 0)
+ *   dtype                               DSDE_FP32 or DSDE_BF16
+ *   V, B, N, k_max                      vocabulary, sequences, drafted positions, SL bound
+ *                                       (1 <= V < 2^31, B >= 1, 0 <= N <= B*k_max,
+ *                                        0 <= k_max <= DSDE_MAX_K)
+ *   sl [B], cu_sl [B+1]     int32       per-sequence SL and its exclusive prefix sums
+ *   draft_tokens [N]        int32       the drafted token at each position
+ *   temperature [B]         float       per-sequence sampling temperature T_b (> 0);
+ *                                       p = softmax(z_target / T_b), q = softmax(z_draft / T_b)
+ *   u_acc [N]               float       acceptance uniforms in [0, 1), one per position
+ *   u_res [B]               float       draw uniforms in [0, 1), one per sequence
+ *   pad_id                              token written into unused slots
+ * Outputs:
+ *   accepted [B]            int32       a_b: number of leading drafted tokens accepted
+ *   tokens [B, k_max+1]     int32       x_0..x_{a_b-1}, the drawn token, then pad_id
+ *   kld [N]                 float       KL(p || q) in nats per drafted position (>= 0)
+ *   seq_err [B]             uint32      DSDE_ERR_* bits per sequence (0 when fine)
+ *   row_lse [N, 2]          double      optional (may be NULL): natural-log normalisers
+ *                                       log sum_v exp(z_v / T_b) of the target and draft rows
+ * The draw walks token ids in ascending order and returns the smallest id whose
+ * cumulative weight exceeds u_res[b] times the total weight.  Acceptance is
+ * evaluated as u < p(x)/q(x) in double precision.
+ */
+int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
+                    int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl,
+                    const int32_t *draft_tokens, const float *temperature, const float *u_acc,
+                    const float *u_res, int32_t pad_id, int32_t *accepted, int32_t *tokens, float *kld,
+                    uint32_t *seq_err, double *row_lse, void *workspace, size_t workspace_bytes,
+                    void *stream);
+
+/*
+ * KLD stability signal (Sec. 3.1.2, Eqs. 3-7).
+ *
+ * For each sequence: if SL_b > 0, mu_last = mean of kld over its SL_b positions
+ * and it is pushed into the sequence's ring (hist[b, head[b]] = mu_last,
+ * head = (head + 1) mod W, count = min(count + 1, W)); if SL_b = 0 nothing is
+ * pushed and mu_last is the newest entry (0 for an empty ring).  Then, over the
+ * n_s = min(n_short, count) and n_l = min(n_long, count) newest entries h_1..h_n
+ * (h_1 newest) with weights alpha_i = delta^(i-1):
+ *   mu_w = sum alpha_i h_i / sum alpha_i,  Var_w = sum alpha_i (h_i - mu_w)^2 / sum alpha_i
+ *   WVIR = Var_s / (Var_l + eps),          SF = exp(2 mu_last) - 1.
+ * An empty window has variance 0.
+ *
+ *   B, N                     sequences and drafted positions (as in dsde_verify)
+ *   sl [B], cu_sl [B+1]      int32   as in dsde_verify
+ *   kld [N]                  float   per-token KLD (dsde_verify's output)
+ *   hist [B, W]              float   ring of per-step mean KLD (in/out)
+ *   head [B], count [B]      int32   next write slot, entries held (in/out)
+ *   W                                ring capacity (>= 1)
+ *   n_short, n_long                  window sizes, 1 <= n_short <= n_long (paper: 10, 30)
+ *   delta                            recency decay in (0, 1] (paper: 0.85)
+ *   eps                              >= 0, added to Var_l (1e-6)
+ * Outputs [B] float: mu_last, var_short, var_long, wvir, sf; seq_err [B] uint32
+ * (DSDE_ERR_LAYOUT, DSDE_ERR_SIGNAL, DSDE_ERR_STATE; a flagged ring is left unchanged).
+ */
+int32_t dsde_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu_sl, const float *kld,
+                        float *hist, int32_t *head, int32_t *count, int32_t W, int32_t n_short,
+                        int32_t n_long, float delta, float eps, float *mu_last, float *var_short,
+                        float *var_long, float *wvir, float *sf, uint32_t *seq_err, void *stream);
+
+/*
+ * Next speculation length with the batch cap (Eqs. 2 and 8; Sec. 3.3, Eqs. 9-11).
+ *
+ *   pen_b   = sf[b] * wvir[b]
+ *   SL_hat_b = (1 - pen_b)(sl_max[b] - sl_min) + sl_min   if pen_b <= 1, else sl_min
+ *   SL_cap  = mean of SL_hat over the sequences without an error (the MSE-optimal cap)
+ *   sl_next[b] = clamp(floor(min(SL_hat_b, SL_cap) + 1/2), ceil(sl_min), sl_hi)
+ * A sequence with a non-finite sf, wvir or sl_max, or sl_max < sl_min, gets
+ * DSDE_ERR_SIGNAL, sl_hat = NaN and sl_next = ceil(sl_min); with no valid
+ * sequence SL_cap is NaN.
+ *
+ *   sf [B], wvir [B], sl_max [B]   float
+ *   sl_min                          finite; ceil(sl_min) <= sl_hi (paper: SL_min = 2)
+ *   sl_hi                           upper bound of the next step's SL (its k_max)
+ * Outputs: sl_hat [B] float, sl_cap [1] float, sl_next [B] int32, seq_err [B] uint32.
+ */
+int32_t dsde_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max, float sl_min,
+                     int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
+                     void *stream);
+
+/*
+ * Profiling hook: when both events are non-NULL (hipEvent_t), every later
+ * dsde_verify records `start` just before and `stop` just after its row
+ * statistics kernel (the pass that reads every drafted row pair once) on its
+ * stream.  Passing NULLs turns it off.  Process-wide; not thread-safe.
+ */
+int32_t dsde_set_profile_events(void *start, void *stop);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DSDE_H_ */

@@ -1,0 +1,184 @@
+"""DSDE speculative-verification hot path on MI355X (gfx950).
+
+Python binding of libdsde.so (declared in include/dsde.h): the same entry
+points, taking torch tensors that already live on the GPU.  This module only
+checks shapes/dtypes and marshals pointers and the current HIP stream; every
+step of the computation runs in the library's HIP kernels.  There is no CPU
+fallback: if the library is missing, ``load`` raises.
+"""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdsde.so")
+
+OK, INVALID_ARG, WORKSPACE_TOO_SMALL, DEVICE_ERROR = 0, 1, 2, 3
+FP32, BF16 = 0, 1
+ERR_LAYOUT, ERR_TOKEN, ERR_LOGIT, ERR_TEMP, ERR_UNIFORM, ERR_SIGNAL, ERR_STATE = 1, 2, 4, 8, 16, 32, 64
+MAX_K = 63
+EXPORTS = ("dsde_abi_version", "dsde_status_string", "dsde_verify_workspace_bytes", "dsde_verify",
+           "dsde_kld_signal", "dsde_next_sl", "dsde_set_profile_events")
+
+_lib = None
+
+
+class DsdeError(RuntimeError):
+    pass
+
+
+def load(path: str = LIB_PATH):
+    """Load libdsde.so (built by ``build_lib.build``); raises when it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise DsdeError(f"{path} is missing: build it with __graft_entry__.build() "
+                        "(there is no fallback implementation)")
+    lib = ctypes.CDLL(path)
+    P, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+    lib.dsde_abi_version.restype = i32
+    lib.dsde_abi_version.argtypes = []
+    lib.dsde_status_string.restype = ctypes.c_char_p
+    lib.dsde_status_string.argtypes = [i32]
+    lib.dsde_verify_workspace_bytes.restype = sz
+    lib.dsde_verify_workspace_bytes.argtypes = [i32, i64, i64, i32]
+    lib.dsde_verify.restype = i32
+    lib.dsde_verify.argtypes = [P, P, i32, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P, P, P, sz, P]
+    lib.dsde_kld_signal.restype = i32
+    lib.dsde_kld_signal.argtypes = [i32, i64, P, P, P, P, P, P, i32, i32, i32, f32, f32, P, P, P, P, P, P, P]
+    lib.dsde_next_sl.restype = i32
+    lib.dsde_next_sl.argtypes = [i32, P, P, P, f32, i32, P, P, P, P, P]
+    lib.dsde_set_profile_events.restype = i32
+    lib.dsde_set_profile_events.argtypes = [P, P]
+    _lib = lib
+    return lib
+
+
+def _check(rc):
+    if rc != OK:
+        raise DsdeError(f"libdsde: {load().dsde_status_string(rc).decode()} (status {rc})")
+
+
+def _ptr(t, dtype=None, n=None, name="tensor"):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise DsdeError(f"{name} must be a GPU tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise DsdeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise DsdeError(f"{name} must be contiguous")
+    if n is not None and t.numel() < n:
+        raise DsdeError(f"{name} has {t.numel()} elements, needs {n}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def workspace_bytes(B, N, V, k_max):
+    return int(load().dsde_verify_workspace_bytes(B, N, V, k_max))
+
+
+def new_workspace(B, N, V, k_max, device="cuda"):
+    n = workspace_bytes(B, N, V, k_max)
+    if n == 0:
+        raise DsdeError("invalid sizes for the verify workspace")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def verify(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, pad_id=-1,
+           out=None, workspace=None, row_lse=None, stream=None):
+    """``dsde_verify`` on torch tensors.  Returns (accepted, tokens, kld, seq_err);
+    pass ``out`` (a dict with those keys) to reuse output buffers."""
+    lib = load()
+    if target.dtype == torch.bfloat16:
+        dt = BF16
+    elif target.dtype == torch.float32:
+        dt = FP32
+    else:
+        raise DsdeError("logits must be bfloat16 or float32")
+    V = int(target.shape[1])
+    B = int(sl.shape[0])
+    N = int(draft.shape[0]) if draft is not None else 0
+    dev = target.device
+    if draft is not None and (draft.dtype != target.dtype or (N > 0 and int(draft.shape[1]) != V)):
+        raise DsdeError("draft logits must match the target's dtype and vocabulary")
+    if int(target.shape[0]) != N + B:
+        raise DsdeError(f"target has {target.shape[0]} rows, expected N + B = {N + B}")
+    if out is None:
+        out = {"accepted": torch.empty(B, dtype=torch.int32, device=dev),
+               "tokens": torch.empty((B, k_max + 1), dtype=torch.int32, device=dev),
+               "kld": torch.empty(max(N, 1), dtype=torch.float32, device=dev)[:N],
+               "seq_err": torch.empty(B, dtype=torch.int32, device=dev)}
+    if workspace is None:
+        workspace = new_workspace(B, N, V, k_max, device=dev)
+    rc = lib.dsde_verify(
+        _ptr(target, name="target"), _ptr(draft, name="draft") if N > 0 else None, dt, V, B, N, k_max,
+        _ptr(sl, torch.int32, B, "sl"), _ptr(cu_sl, torch.int32, B + 1, "cu_sl"),
+        _ptr(draft_tokens, torch.int32, N, "draft_tokens") if N > 0 else None,
+        _ptr(temperature, torch.float32, B, "temperature"),
+        _ptr(u_acc, torch.float32, N, "u_acc") if N > 0 else None,
+        _ptr(u_res, torch.float32, B, "u_res"), int(pad_id),
+        _ptr(out["accepted"], torch.int32, B, "accepted"),
+        _ptr(out["tokens"], torch.int32, B * (k_max + 1), "tokens"),
+        _ptr(out["kld"], torch.float32, N, "kld") if N > 0 else None,
+        _ptr(out["seq_err"], None, B, "seq_err"),
+        _ptr(row_lse, torch.float64, 2 * N, "row_lse") if row_lse is not None else None,
+        _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc)
+    return out
+
+
+def kld_signal(sl, cu_sl, kld, hist, head, count, n_short=10, n_long=30, delta=0.85, eps=1e-6,
+               out=None, stream=None):
+    """``dsde_kld_signal``: updates hist/head/count in place; returns the outputs."""
+    lib = load()
+    B = int(sl.shape[0])
+    N = int(kld.shape[0])
+    W = int(hist.shape[1])
+    dev = sl.device
+    if out is None:
+        out = {k: torch.empty(B, dtype=torch.float32, device=dev)
+               for k in ("mu_last", "var_short", "var_long", "wvir", "sf")}
+        out["seq_err"] = torch.empty(B, dtype=torch.int32, device=dev)
+    rc = lib.dsde_kld_signal(
+        B, N, _ptr(sl, torch.int32, B, "sl"), _ptr(cu_sl, torch.int32, B + 1, "cu_sl"),
+        _ptr(kld, torch.float32, N, "kld") if N > 0 else None, _ptr(hist, torch.float32, B * W, "hist"),
+        _ptr(head, torch.int32, B, "head"), _ptr(count, torch.int32, B, "count"), W, n_short, n_long,
+        float(delta), float(eps), _ptr(out["mu_last"], torch.float32, B), _ptr(out["var_short"], torch.float32, B),
+        _ptr(out["var_long"], torch.float32, B), _ptr(out["wvir"], torch.float32, B),
+        _ptr(out["sf"], torch.float32, B), _ptr(out["seq_err"], None, B), _stream(stream))
+    _check(rc)
+    return out
+
+
+def next_sl(sf, wvir, sl_max, sl_min=2.0, sl_hi=8, out=None, stream=None):
+    """``dsde_next_sl``: SL rule with the batch cap; returns sl_hat, sl_cap, sl_next, seq_err."""
+    lib = load()
+    B = int(sf.shape[0])
+    dev = sf.device
+    if out is None:
+        out = {"sl_hat": torch.empty(B, dtype=torch.float32, device=dev),
+               "sl_cap": torch.empty(1, dtype=torch.float32, device=dev),
+               "sl_next": torch.empty(B, dtype=torch.int32, device=dev),
+               "seq_err": torch.empty(B, dtype=torch.int32, device=dev)}
+    rc = lib.dsde_next_sl(B, _ptr(sf, torch.float32, B, "sf"), _ptr(wvir, torch.float32, B, "wvir"),
+                          _ptr(sl_max, torch.float32, B, "sl_max"), float(sl_min), int(sl_hi),
+                          _ptr(out["sl_hat"], torch.float32, B), _ptr(out["sl_cap"], torch.float32, 1),
+                          _ptr(out["sl_next"], torch.int32, B), _ptr(out["seq_err"], None, B), _stream(stream))
+    _check(rc)
+    return out
+
+
+def set_profile_events(start=None, stop=None):
+    """Record torch.cuda.Event ``start``/``stop`` around the row-statistics kernel of
+    every later ``verify`` call (None, None turns it off)."""
+    lib = load()
+    s = ctypes.c_void_p(start.cuda_event) if start is not None else None
+    e = ctypes.c_void_p(stop.cuda_event) if stop is not None else None
+    _check(lib.dsde_set_profile_events(s, e))

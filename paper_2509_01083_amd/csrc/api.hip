@@ -1,0 +1,117 @@
+// C ABI of libdsde: host-side argument validation (before any HIP call),
+// workspace sizing and dispatch to the kernels.
+#include <math.h>
+
+#include "common.hpp"
+
+namespace {
+
+hipEvent_t g_prof_start = nullptr, g_prof_stop = nullptr;
+
+bool verify_sizes_ok(int32_t B, int64_t N, int64_t V, int32_t k_max) {
+  if (B < 1 || V < 1 || V >= (int64_t(1) << 31) || N < 0 || k_max < 0 || k_max > DSDE_MAX_K) return false;
+  if (N > int64_t(B) * k_max) return false;
+  const int64_t nc = (V + dsde::kChunk - 1) / dsde::kChunk;
+  // grid sizes of the row kernels must fit one launch dimension
+  if (N * nc >= (int64_t(1) << 31) || int64_t(B) * nc >= (int64_t(1) << 31)) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t dsde_abi_version(void) { return DSDE_ABI_VERSION; }
+
+const char *dsde_status_string(int32_t status) {
+  switch (status) {
+    case DSDE_OK:
+      return "ok";
+    case DSDE_INVALID_ARG:
+      return "invalid argument";
+    case DSDE_WORKSPACE_TOO_SMALL:
+      return "workspace too small";
+    case DSDE_DEVICE_ERROR:
+      return "device error";
+    default:
+      return "unknown status";
+  }
+}
+
+size_t dsde_verify_workspace_bytes(int32_t B, int64_t N, int64_t V, int32_t k_max) {
+  if (!verify_sizes_ok(B, N, V, k_max)) return 0;
+  return dsde::workspace_layout(B, N, V).total;
+}
+
+int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
+                    int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl,
+                    const int32_t *draft_tokens, const float *temperature, const float *u_acc,
+                    const float *u_res, int32_t pad_id, int32_t *accepted, int32_t *tokens, float *kld,
+                    uint32_t *seq_err, double *row_lse, void *workspace, size_t workspace_bytes,
+                    void *stream) {
+  if (dtype != DSDE_FP32 && dtype != DSDE_BF16) return DSDE_INVALID_ARG;
+  if (!verify_sizes_ok(B, N, V, k_max)) return DSDE_INVALID_ARG;
+  if (!target_logits || !sl || !cu_sl || !temperature || !u_res || !accepted || !tokens || !seq_err ||
+      !workspace)
+    return DSDE_INVALID_ARG;
+  if (N > 0 && (!draft_logits || !draft_tokens || !u_acc || !kld)) return DSDE_INVALID_ARG;
+  if (workspace_bytes < dsde::workspace_layout(B, N, V).total) return DSDE_WORKSPACE_TOO_SMALL;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return DSDE_INVALID_ARG;
+  dsde::VerifyArgs a;
+  a.target = target_logits;
+  a.draft = draft_logits;
+  a.dtype = dtype;
+  a.V = V;
+  a.B = B;
+  a.N = N;
+  a.k_max = k_max;
+  a.sl = sl;
+  a.cu_sl = cu_sl;
+  a.draft_tokens = draft_tokens;
+  a.temperature = temperature;
+  a.u_acc = u_acc;
+  a.u_res = u_res;
+  a.pad_id = pad_id;
+  a.accepted = accepted;
+  a.tokens = tokens;
+  a.kld = kld;
+  a.seq_err = seq_err;
+  a.row_lse = row_lse;
+  a.workspace = workspace;
+  a.stream = static_cast<hipStream_t>(stream);
+  a.prof_start = g_prof_start;
+  a.prof_stop = g_prof_stop;
+  return dsde::launch_verify(a);
+}
+
+int32_t dsde_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu_sl, const float *kld,
+                        float *hist, int32_t *head, int32_t *count, int32_t W, int32_t n_short,
+                        int32_t n_long, float delta, float eps, float *mu_last, float *var_short,
+                        float *var_long, float *wvir, float *sf, uint32_t *seq_err, void *stream) {
+  if (B < 1 || N < 0 || W < 1 || n_short < 1 || n_short > n_long) return DSDE_INVALID_ARG;
+  if (!(delta > 0.0f && delta <= 1.0f) || !(eps >= 0.0f) || !isfinite(eps)) return DSDE_INVALID_ARG;
+  if (!sl || !cu_sl || !hist || !head || !count || !mu_last || !var_short || !var_long || !wvir || !sf ||
+      !seq_err)
+    return DSDE_INVALID_ARG;
+  if (N > 0 && !kld) return DSDE_INVALID_ARG;
+  return dsde::launch_kld_signal(B, N, sl, cu_sl, kld, hist, head, count, W, n_short, n_long, delta, eps, mu_last,
+                                 var_short, var_long, wvir, sf, seq_err, static_cast<hipStream_t>(stream));
+}
+
+int32_t dsde_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max, float sl_min,
+                     int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
+                     void *stream) {
+  if (B < 1 || !isfinite(sl_min) || ceilf(sl_min) > float(sl_hi)) return DSDE_INVALID_ARG;
+  if (!sf || !wvir || !sl_max || !sl_hat || !sl_cap || !sl_next || !seq_err) return DSDE_INVALID_ARG;
+  return dsde::launch_next_sl(B, sf, wvir, sl_max, sl_min, sl_hi, sl_hat, sl_cap, sl_next, seq_err,
+                              static_cast<hipStream_t>(stream));
+}
+
+int32_t dsde_set_profile_events(void *start, void *stop) {
+  if ((start == nullptr) != (stop == nullptr)) return DSDE_INVALID_ARG;
+  g_prof_start = static_cast<hipEvent_t>(start);
+  g_prof_stop = static_cast<hipEvent_t>(stop);
+  return DSDE_OK;
+}
+
+}  // extern "C"

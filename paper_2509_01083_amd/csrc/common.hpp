@@ -1,0 +1,110 @@
+// Internal definitions shared by the HIP translation units of libdsde.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dsde.h"
+
+namespace dsde {
+
+constexpr int kThreads = 256;              // threads per workgroup of the row kernels (4 wavefronts)
+constexpr int kWaves = kThreads / 64;
+constexpr int kEltsPerThread = 32;         // logits per row per thread in one chunk
+constexpr int kChunk = kThreads * kEltsPerThread;  // logits per row chunk (8192)
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr double kLn2 = 0.6931471805599453;
+
+// Per drafted position, written by the set-up kernel: the target row of the
+// pair (-1 when its sequence is flagged) and the log2-domain scale
+// c = log2(e) / T_b as raw float bits.
+struct PairInfo {
+  int32_t target_row;
+  int32_t scale_bits;
+};
+
+// Row statistics of one chunk of one drafted row pair.  Every sum is taken
+// relative to the chunk's own reference shifts mt, md (log2 domain):
+//   sp = sum 2^(z_t c - mt),   sq = sum 2^(z_d c - md),
+//   a  = sum 2^(z_t c - mt) * ((z_t c - mt) - (z_d c - md)).
+struct alignas(16) PairChunk {
+  float mt, md;
+  float pad0, pad1;
+  double sp, sq, a;
+  double pad2;
+};
+
+// What the draw of one sequence needs, written by the acceptance kernel.
+struct alignas(16) DrawJob {
+  int32_t kind;        // 0: residual of a rejected pair, 1: bonus row, -1: nothing (flagged)
+  int32_t accepted;    // a_b
+  int32_t target_row;
+  int32_t draft_row;   // -1 for the bonus row
+  float scale;         // c = log2(e) / T_b
+  float mt, md;        // row reference shifts of the rejected pair
+  float inv_sp, inv_sq;  // 1 / row sums of the rejected pair
+  float u;             // draw uniform
+  int32_t pad0, pad1;
+};
+
+// Chunk totals of the draw weights.  Residual: w = max(0, p - q) and the
+// fallback p; bonus: e = 2^(z c - ref) relative to the chunk reference.
+struct alignas(16) DrawChunk {
+  double w;
+  double p;    // residual: sum of p over the chunk (used when the residual mass is 0)
+  float ref;   // bonus: chunk reference shift
+  int32_t bad; // bonus: a NaN or +-inf logit was seen
+  int32_t pad0, pad1;
+};
+
+inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct WorkspaceLayout {
+  size_t pair_info, pair_chunk, draw_job, draw_chunk, total;
+};
+
+inline WorkspaceLayout workspace_layout(int32_t B, int64_t N, int64_t V) {
+  const int64_t nc = (V + kChunk - 1) / kChunk;
+  WorkspaceLayout L;
+  size_t off = 0;
+  L.pair_info = off;
+  off += align_up(sizeof(PairInfo) * size_t(N > 0 ? N : 1));
+  L.pair_chunk = off;
+  off += align_up(sizeof(PairChunk) * size_t(N > 0 ? N : 1) * size_t(nc));
+  L.draw_job = off;
+  off += align_up(sizeof(DrawJob) * size_t(B));
+  L.draw_chunk = off;
+  off += align_up(sizeof(DrawChunk) * size_t(B) * size_t(nc));
+  L.total = off;
+  return L;
+}
+
+struct VerifyArgs {
+  const void *target, *draft;
+  int32_t dtype;
+  int64_t V;
+  int32_t B;
+  int64_t N;
+  int32_t k_max;
+  const int32_t *sl, *cu_sl, *draft_tokens;
+  const float *temperature, *u_acc, *u_res;
+  int32_t pad_id;
+  int32_t *accepted, *tokens;
+  float *kld;
+  uint32_t *seq_err;
+  double *row_lse;
+  void *workspace;
+  hipStream_t stream;
+  hipEvent_t prof_start, prof_stop;
+};
+
+int launch_verify(const VerifyArgs &a);
+int launch_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu_sl, const float *kld,
+                      float *hist, int32_t *head, int32_t *count, int32_t W, int32_t n_short, int32_t n_long,
+                      float delta, float eps, float *mu_last, float *var_short, float *var_long, float *wvir,
+                      float *sf, uint32_t *seq_err, hipStream_t stream);
+int launch_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max, float sl_min,
+                   int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
+                   hipStream_t stream);
+
+}  // namespace dsde

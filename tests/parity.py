@@ -1,0 +1,76 @@
+"""Comparison rules between the HIP path and the CPU oracle.
+
+Bit-exact: per-sequence error bits, accepted counts and emitted tokens of every
+sequence whose decisions are not ties (the oracle flags a sequence when an
+acceptance test lies within 1e-6 of u, or the drawn token's CDF boundary lies
+within 1e-6 probability mass of u' * Z).  Tie sequences are counted and checked
+only for validity (accepted drafts are a prefix of the drafted tokens, the rest
+is padding).
+
+Floating point: KLD within 1e-4 relative plus 1e-6 absolute.  The absolute
+floor comes from fp32 arithmetic: each log-probability difference entering KL
+is formed from fp32 values of magnitude up to ~10 (unit roundoff 6e-8), so a
+KL near 0 carries an absolute error of order 1e-7..1e-6.
+"""
+import numpy as np
+
+KLD_REL, KLD_ABS = 1e-4, 1e-6
+LSE_ABS = 2e-5
+
+
+def run_verify(dsde, step, row_lse=True):
+    import torch
+    lse = torch.empty((max(step.N, 1), 2), dtype=torch.float64, device=step.target.device)[:step.N] \
+        if row_lse else None
+    out = dsde.verify(step.target, step.draft, step.sl, step.cu_sl, step.draft_tokens, step.temperature,
+                      step.u_acc, step.u_res, step.k_max, row_lse=lse)
+    torch.cuda.synchronize()
+    res = {k: v.cpu().numpy() for k, v in out.items()}
+    if lse is not None:
+        res["row_lse"] = lse.cpu().numpy()
+    return res
+
+
+def compare_verify(got, ref, sl, cu_sl, label=""):
+    """Asserts the comparison rules; returns a small report."""
+    B = len(sl)
+    err_g = got["seq_err"].astype(np.uint32)
+    err_r = ref["seq_err"].astype(np.uint32)
+    assert np.array_equal(err_g, err_r), f"{label}: error bits differ: {np.nonzero(err_g != err_r)[0][:10]}"
+    fine = err_r == 0
+    ties = (ref["acc_tie"] != 0) | (ref["cdf_tie"] != 0)
+    cmp = fine & ~ties
+    bad_acc = np.nonzero(cmp & (got["accepted"] != ref["accepted"]))[0]
+    assert bad_acc.size == 0, f"{label}: accepted differs at {bad_acc[:10]}: " \
+                              f"{got['accepted'][bad_acc[:5]]} vs {ref['accepted'][bad_acc[:5]]}"
+    bad_tok = np.nonzero(cmp & (got["tokens"] != ref["tokens"]).any(axis=1))[0]
+    assert bad_tok.size == 0, f"{label}: tokens differ at {bad_tok[:10]}"
+    # tie sequences: outputs are still a valid emission
+    for b in np.nonzero(fine & ties)[0]:
+        a = int(got["accepted"][b])
+        assert 0 <= a <= sl[b]
+        toks = got["tokens"][b]
+        assert (toks[a + 1:] == -1).all()
+    # errored sequences get the defined fallback
+    for b in np.nonzero(~fine)[0]:
+        assert got["accepted"][b] == 0 and (got["tokens"][b] == -1).all()
+    # KLD
+    N = int(cu_sl[-1]) if len(cu_sl) else 0
+    pos_fine = np.repeat(fine, sl) if N == len(ref["kld"]) else np.zeros(len(ref["kld"]), bool)
+    kg = got["kld"].astype(np.float64)
+    kr = ref["kld"]
+    if pos_fine.any():
+        d = np.abs(kg[pos_fine] - kr[pos_fine])
+        lim = KLD_REL * np.abs(kr[pos_fine]) + KLD_ABS
+        worst = int(np.argmax(d - lim))
+        assert (d <= lim).all(), f"{label}: kld off by {d[worst]:.3g} (ref {kr[pos_fine][worst]:.6g})"
+    report = {"B": B, "compared": int(cmp.sum()), "acc_ties": int((ref["acc_tie"] != 0).sum()),
+              "cdf_ties": int((ref["cdf_tie"] != 0).sum()), "errored": int((~fine).sum())}
+    if "row_lse" in got and pos_fine.any():
+        dl = np.abs(got["row_lse"][pos_fine] - ref["lse"][pos_fine])
+        report["lse_max_abs_err"] = float(dl.max())
+        assert dl.max() <= LSE_ABS, f"{label}: row lse off by {dl.max():.3g}"
+    if pos_fine.any():
+        report["kld_max_rel_err"] = float((np.abs(kg[pos_fine] - kr[pos_fine]) /
+                                           np.maximum(np.abs(kr[pos_fine]), 1e-12)).max())
+    return report

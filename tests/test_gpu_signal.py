@@ -1,0 +1,193 @@
+"""GPU parity of dsde_kld_signal and dsde_next_sl against the CPU oracle, alone
+and chained behind dsde_verify (including the multi-step controller loop).
+
+Tolerances: mu_last, SF, WVIR, SL_hat and the cap within 1e-4 relative;
+variances within 1e-4 relative plus 1e-9 absolute.  SL decisions are
+bit-exact except where the oracle's tie analysis flags them: in isolation
+(identical float inputs) only decisions within 1e-5 of a rounding boundary;
+behind dsde_verify, also decisions that a relative change of 1e-4 in any KLD
+history entry (the KLD tolerance) could flip.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from tests.helpers import packed_layout
+from tests.parity import compare_verify, run_verify
+
+pytestmark = pytest.mark.gpu
+
+REL = 1e-4
+
+
+def announce(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+def close(got, ref, rel=REL, abs_=0.0, label=""):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    bad = ~(np.abs(got - ref) <= rel * np.abs(ref) + abs_)
+    bad &= ~(np.isnan(got) & np.isnan(ref))
+    assert not bad.any(), f"{label}: {np.nonzero(bad)[0][:8]} got {got[bad][:4]} ref {ref[bad][:4]}"
+
+
+def gpu_signal(dsde, sl, cu, kld, st, n_short=10, n_long=30, delta=0.85, eps=1e-6):
+    out = dsde.kld_signal(sl, cu, kld, st.hist, st.head, st.count, n_short, n_long, delta, eps)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def compare_signal(got, ref, label):
+    assert np.array_equal(got["seq_err"].astype(np.uint32), ref["seq_err"]), label
+    for k in ("mu_last", "sf", "wvir"):
+        close(got[k], ref[k], label=f"{label} {k}")
+    for k in ("var_short", "var_long"):
+        close(got[k], ref[k], abs_=1e-9, label=f"{label} {k}")
+
+
+@pytest.mark.parametrize("W_, n_short, n_long", [(32, 10, 30), (8, 10, 30), (16, 3, 12), (40, 10, 30)])
+def test_kld_signal_alone(gpu_lib, W_, n_short, n_long):
+    announce(f"kld_signal W={W_} windows={n_short}/{n_long}")
+    rng = np.random.default_rng(W_)
+    B = 300
+    sls = rng.integers(0, 9, B)
+    sl, cu = packed_layout(sls)
+    kld = (rng.gamma(0.6, 0.5, int(cu[-1]))).astype(np.float32)
+    cfg = dict(W.CONFIGS["b256"], B=B, W=W_)
+    st = W.make_signal_state(cfg, seed=3, device="cuda")
+    # a few partly filled and empty rings
+    cnt = st.count.cpu().numpy()
+    cnt[::7] = rng.integers(0, W_ + 1, len(cnt[::7]))
+    cnt[5] = 0
+    st.count.copy_(torch.as_tensor(cnt))
+    h0, hd0, c0 = st.hist.cpu().numpy(), st.head.cpu().numpy(), st.count.cpu().numpy()
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    got = gpu_signal(gpu_lib, dev(sl), dev(cu), dev(kld), st, n_short, n_long)
+    ref = oracle.kld_signal(sl, cu, kld.astype(np.float64), h0, hd0, c0, n_short, n_long)
+    compare_signal(got, ref, "signal")
+    assert np.array_equal(st.head.cpu().numpy(), ref["head"])
+    assert np.array_equal(st.count.cpu().numpy(), ref["count"])
+    close(st.hist.cpu().numpy(), ref["hist"], rel=1e-7, label="ring")
+
+
+def test_kld_signal_errors(gpu_lib):
+    announce("kld_signal errors")
+    sls = [2, 0, 3, 1]
+    sl, cu = packed_layout(sls)
+    kld = np.array([0.1, 0.2, np.nan, 0.3, 0.4, 0.5], np.float32)
+    cfg = dict(W.CONFIGS["b64"], B=4)
+    st = W.make_signal_state(cfg, seed=1, device="cuda")
+    st.head[3] = 99  # bad ring state
+    h0, hd0, c0 = st.hist.cpu().numpy(), st.head.cpu().numpy(), st.count.cpu().numpy()
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    got = gpu_signal(gpu_lib, dev(sl), dev(cu), dev(kld), st)
+    ref = oracle.kld_signal(sl, cu, kld.astype(np.float64), h0, hd0, c0)
+    assert list(got["seq_err"]) == [0, 0, 32, 64]
+    compare_signal(got, ref, "signal errors")
+    cu_bad = cu.copy()
+    cu_bad[2] += 1
+    got = gpu_signal(gpu_lib, dev(sl), dev(cu_bad), dev(kld), st)
+    assert (got["seq_err"] == 1).all()
+
+
+def sl_decision_ties(hat, cap, seq_err, sl_min, sl_hi, tau=1e-5):
+    return oracle.sl_round_ties(hat, np.zeros_like(hat), seq_err, sl_min, sl_hi, tau)
+
+
+def test_next_sl_alone(gpu_lib):
+    announce("next_sl")
+    rng = np.random.default_rng(9)
+    B = 2000
+    sf = (rng.gamma(0.5, 0.6, B)).astype(np.float32)
+    wvir = (rng.gamma(1.0, 0.8, B)).astype(np.float32)
+    sl_max = rng.choice([8.0, 16.0, 6.5], B).astype(np.float32)
+    sf[7] = np.nan
+    sl_max[11] = 1.0  # below sl_min
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    out = gpu_lib.next_sl(dev(sf), dev(wvir), dev(sl_max), 2.0, 16)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    ref = oracle.next_sl(sf.astype(np.float64), wvir.astype(np.float64), sl_max.astype(np.float64), 2.0, 16)
+    assert np.array_equal(got["seq_err"].astype(np.uint32), ref["seq_err"])
+    close(got["sl_hat"], ref["sl_hat"], label="sl_hat")
+    close(got["sl_cap"], [ref["sl_cap"]], label="cap")
+    ties = sl_decision_ties(ref["sl_hat"], ref["sl_cap"], ref["seq_err"], 2.0, 16)
+    ok = ties == 0
+    assert np.array_equal(got["sl_next"][ok], ref["sl_next"][ok])
+    print(f"[report] next_sl ties={int(ties.sum())} of {B}", flush=True)
+
+
+def chained_step(dsde, step, st, sl_max, sl_hi, label):
+    """verify -> kld_signal -> next_sl on the GPU and the oracle's chain; compares every stage."""
+    h0, hd0, c0 = st.hist.cpu().numpy(), st.head.cpu().numpy(), st.count.cpu().numpy()
+    got = run_verify(dsde, step, row_lse=False)
+    host = W.host_arrays(step)
+    ref = oracle.verify(**host, n_threads=16)
+    rep = compare_verify(got, ref, host["sl"], host["cu_sl"], label)
+    kld_t = torch.as_tensor(got["kld"], device="cuda")
+    sg = gpu_signal(dsde, step.sl, step.cu_sl, kld_t, st)
+    sr = oracle.kld_signal(host["sl"], host["cu_sl"], ref["kld"], h0, hd0, c0)
+    # sequences the verify flagged have NaN KLD on both sides
+    compare_signal(sg, sr, f"{label} signal")
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    out = dsde.next_sl(dev(sg["sf"]), dev(sg["wvir"]), sl_max, 2.0, sl_hi)
+    torch.cuda.synchronize()
+    ng = {k: v.cpu().numpy() for k, v in out.items()}
+    smax = sl_max.cpu().numpy().astype(np.float64)
+    nr = oracle.next_sl(sr["sf"], sr["wvir"], smax, 2.0, sl_hi)
+    assert np.array_equal(ng["seq_err"].astype(np.uint32), nr["seq_err"])
+    close(ng["sl_hat"], nr["sl_hat"], rel=1e-3, label=f"{label} sl_hat")
+    hat, dhat = oracle.sl_hat_spread(sr["hist"], sr["head"], sr["count"], smax, nr["seq_err"], rho=1e-4)
+    ties = oracle.sl_round_ties(hat, dhat, nr["seq_err"], 2.0, sl_hi, tau=1e-5)
+    ok = ties == 0
+    mism = np.nonzero(ok & (ng["sl_next"] != nr["sl_next"]))[0]
+    assert mism.size == 0, f"{label}: SL decisions differ at {mism[:8]}"
+    rep["sl_ties"] = int(ties.sum())
+    return ng, nr, sr, rep
+
+
+@pytest.mark.parametrize("name", ["tiny", "b64", "b256", "lowacc"])
+def test_chained_step(gpu_lib, name):
+    cfg = W.CONFIGS[name]
+    step = W.make_step(cfg, seed=21, device="cuda")
+    st = W.make_signal_state(cfg, seed=21, device="cuda")
+    announce(f"chained {name} B={step.B} N={step.N} V={step.V}")
+    _, _, _, rep = chained_step(gpu_lib, step, st, st.sl_max, cfg["k_max"], name)
+    print(f"[report] chained {name}: {rep}", flush=True)
+
+
+def run_loop(dsde, cfg, steps, seed, label):
+    """The multi-step controller: each step's SLs come from the previous step's
+    decisions.  Both sides use the oracle's decisions to build the next step,
+    so a tie can never fork the two trajectories; the GPU decisions are compared
+    at every step."""
+    B = cfg["B"]
+    st = W.make_signal_state(cfg, seed=seed, device="cuda")
+    sl = W.sample_sl(cfg, seed)
+    sigma = W.initial_sigma(cfg, seed)
+    total_ties, total_cmp = 0, 0
+    for t in range(steps):
+        step = W.make_step(cfg, seed=seed, device="cuda", step=t, sl=sl, sigma=sigma)
+        ng, nr, sr, rep = chained_step(dsde, step, st, st.sl_max, cfg["k_max"], f"{label} step {t}")
+        total_ties += rep["sl_ties"]
+        total_cmp += B
+        # keep the GPU ring in step with the oracle ring (fp32 copy of it)
+        st.hist.copy_(torch.as_tensor(sr["hist"].astype(np.float32)))
+        sl = nr["sl_next"]
+        sigma = W.walk_sigma(sigma, cfg, seed, t)
+    print(f"[report] {label}: {steps} steps, SL ties {total_ties} of {total_cmp}", flush=True)
+
+
+def test_controller_loop_reduced_vocab(gpu_lib):
+    cfg = dict(W.CONFIGS["loop"], B=256, V=4096)
+    announce("controller loop B=256 V=4096 200 steps")
+    run_loop(gpu_lib, cfg, 200, seed=5, label="loop-reduced")
+
+
+def test_controller_loop_full_shape(gpu_lib):
+    cfg = W.CONFIGS["loop"]
+    announce("controller loop B=1024 V=128256 3 steps")
+    run_loop(gpu_lib, cfg, 3, seed=6, label="loop-full")

@@ -1,0 +1,192 @@
+"""GPU parity of dsde_verify against the CPU oracle (through the C ABI).
+
+Inputs are seeded and synthetic (workloads.py); the oracle receives a host copy
+of the very same device inputs.  Every case prints its name before it runs.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from tests.helpers import bf16_bits, packed_layout
+from tests.parity import compare_verify, run_verify
+
+pytestmark = pytest.mark.gpu
+
+
+def announce(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+def check_step(dsde, step, label, n_threads=16):
+    announce(f"{label}: B={step.B} N={step.N} V={step.V} dtype={step.target.dtype}")
+    got = run_verify(dsde, step)
+    ref = oracle.verify(**W.host_arrays(step), n_threads=n_threads)
+    rep = compare_verify(got, ref, W.host_arrays(step)["sl"], step.cu_sl.cpu().numpy(), label)
+    print(f"[report] {label}: {rep}", flush=True)
+    return got, ref, rep
+
+
+def step_from_arrays(target, draft, sls, tokens, temps, u_acc, u_res, k_max, dtype="bf16", device="cuda"):
+    sl, cu = packed_layout(sls)
+    tt = torch.float32 if dtype == "fp32" else torch.bfloat16
+
+    def dev(x):
+        return torch.as_tensor(np.ascontiguousarray(x), device=device)
+    return W.Step(target=dev(target.astype(np.float32)).to(tt), draft=dev(draft.astype(np.float32)).to(tt),
+                  sl=dev(sl), cu_sl=dev(cu), draft_tokens=dev(np.asarray(tokens, np.int32)),
+                  temperature=dev(np.asarray(temps, np.float32)), u_acc=dev(np.asarray(u_acc, np.float32)),
+                  u_res=dev(np.asarray(u_res, np.float32)), k_max=k_max)
+
+
+def random_arrays(rng, sls, V, sigma=2.0, noise=1.0):
+    sl, cu = packed_layout(sls)
+    B, N = len(sls), int(cu[-1])
+    target = rng.normal(0, sigma, (N + B, V)).astype(np.float32)
+    seq = np.repeat(np.arange(B), sls)
+    draft = (target[np.arange(N) + seq] + rng.normal(0, noise, (N, V))).astype(np.float32)
+    tokens = rng.integers(0, V, N)
+    return target, draft, tokens, rng.random(N).astype(np.float32), rng.random(B).astype(np.float32)
+
+
+@pytest.mark.parametrize("name", ["tiny", "b64", "b256", "lowacc"])
+def test_workload_parity(gpu_lib, name):
+    cfg = W.CONFIGS[name]
+    step = W.make_step(cfg, seed=11, device="cuda")
+    _, ref, rep = check_step(gpu_lib, step, f"workload {name}")
+    assert rep["compared"] >= 0.9 * step.B
+
+
+@pytest.mark.parametrize("V", [1, 2, 17, 100, 8191, 8200, 16392, 32001])
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_vocab_edges(gpu_lib, V, dtype):
+    rng = np.random.default_rng(V)
+    sls = [3, 0, 1, 5, 2, 0, 4]
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V, noise=0.7)
+    step = step_from_arrays(target, draft, sls, tokens, [1.0, 0.7, 1.3, 1.0, 0.5, 2.0, 1.0], u_acc, u_res, 5,
+                            dtype)
+    check_step(gpu_lib, step, f"vocab V={V} {dtype}")
+
+
+def test_nothing_drafted(gpu_lib):
+    rng = np.random.default_rng(3)
+    V = 5000
+    target = rng.normal(0, 2, (6, V)).astype(np.float32)
+    step = step_from_arrays(target, np.zeros((0, V), np.float32), [0] * 6, [], [1.0] * 6, [], rng.random(6), 4)
+    got, _, rep = check_step(gpu_lib, step, "all SL = 0")
+    assert (got["accepted"] == 0).all() and rep["compared"] + rep["cdf_ties"] == 6
+
+
+def test_identical_rows_accept_everything_with_zero_kld(gpu_lib):
+    rng = np.random.default_rng(4)
+    sls = [4, 2, 3]
+    V = 12345
+    target, _, tokens, u_acc, u_res = random_arrays(rng, sls, V)
+    sl, cu = packed_layout(sls)
+    seq = np.repeat(np.arange(3), sls)
+    draft = target[np.arange(cu[-1]) + seq]
+    u_acc = np.full(cu[-1], np.float32(np.nextafter(np.float32(1), np.float32(0))))
+    step = step_from_arrays(target, draft, sls, tokens, [1.0, 0.8, 1.2], u_acc, u_res, 4)
+    got, _, _ = check_step(gpu_lib, step, "identical rows")
+    assert (got["accepted"] == np.array(sls)).all()
+    assert (got["kld"] == 0.0).all()
+
+
+def test_peaked_distributions(gpu_lib):
+    rng = np.random.default_rng(5)
+    sls = [3, 3, 3, 3]
+    V = 20000
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V)
+    target[:, 77] += 60.0            # p is one-hot at 77
+    draft[0::2, 77] += 60.0          # q one-hot at 77 on even positions
+    draft[1::2, 123] += 60.0         # and at 123 on odd ones
+    tokens[:] = np.where(np.arange(len(tokens)) % 2 == 0, 77, 123)
+    step = step_from_arrays(target, draft, sls, tokens, [1.0] * 4, u_acc, u_res, 3)
+    check_step(gpu_lib, step, "peaked p and q")
+
+
+def test_error_contract(gpu_lib):
+    rng = np.random.default_rng(6)
+    sls = [2, 2, 2, 2, 2, 2, 2]
+    V = 9000
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V)
+    temps = np.ones(7, np.float32)
+    tokens[2] = V                  # seq 1: token out of range
+    u_acc[4] = 1.0                 # seq 2: uniform out of [0, 1)
+    temps[3] = -1.0                # seq 3: temperature
+    draft[8, 17] = np.nan          # seq 4: NaN in a drafted pair
+    target[5 * 3 + 1, 40] = -np.inf  # seq 5: -inf in a drafted target row
+    # seq 6: both drafts accepted (equal rows, u just below 1), bonus row has +inf
+    target[6 * 3: 6 * 3 + 2] = draft[12:14]
+    u_acc[12:14] = 0.99999
+    target[6 * 3 + 2, 5] = np.inf
+    step = step_from_arrays(target, draft, sls, tokens, temps, u_acc, u_res, 2)
+    got, ref, _ = check_step(gpu_lib, step, "error contract")
+    assert list(got["seq_err"]) == [0, 2, 16, 8, 4, 4, 4]
+    assert np.isnan(got["kld"][2:]).all() and np.isfinite(got["kld"][:2]).all()
+
+
+def test_bad_layout(gpu_lib):
+    rng = np.random.default_rng(7)
+    sls = [2, 3, 1]
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, 500)
+    step = step_from_arrays(target, draft, sls, tokens, [1.0] * 3, u_acc, u_res, 3)
+    cu = step.cu_sl.clone()
+    cu[1] += 1
+    step.cu_sl = cu
+    announce("bad layout")
+    got = run_verify(gpu_lib, step, row_lse=False)
+    assert (got["seq_err"] == 1).all() and (got["accepted"] == 0).all() and (got["tokens"] == -1).all()
+
+
+def test_unaligned_rows_take_the_scalar_path(gpu_lib):
+    rng = np.random.default_rng(8)
+    sls = [3, 1, 4]
+    V = 4096
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V, noise=0.5)
+    step = step_from_arrays(target, draft, sls, tokens, [1.0, 0.7, 1.0], u_acc, u_res, 4)
+    # the same logits, one element past a 16-byte boundary
+    tb = torch.empty(step.target.numel() + 1, dtype=torch.bfloat16, device="cuda")
+    db = torch.empty(step.draft.numel() + 1, dtype=torch.bfloat16, device="cuda")
+    tb[1:].copy_(step.target.reshape(-1))
+    db[1:].copy_(step.draft.reshape(-1))
+    shifted = W.Step(**{**step.__dict__, "target": tb[1:].view(step.target.shape),
+                        "draft": db[1:].view(step.draft.shape)})
+    check_step(gpu_lib, shifted, "unaligned rows")
+
+
+def test_deterministic(gpu_lib):
+    step = W.make_step(W.CONFIGS["b64"], seed=12, device="cuda")
+    announce("determinism b64")
+    a = run_verify(gpu_lib, step)
+    b = run_verify(gpu_lib, step)
+    for k in ("accepted", "tokens", "seq_err", "row_lse"):
+        assert np.array_equal(a[k], b[k]), k
+    assert np.array_equal(a["kld"].view(np.uint32), b["kld"].view(np.uint32))
+
+
+def test_draw_distribution_matches_target(gpu_lib):
+    """Speculative-sampling theorem on the GPU: over a grid of uniforms the
+    emitted first token is distributed as p (no oracle involved)."""
+    V, M = 7, 64
+    zt = np.array([0.5, -1.0, 1.5, 0.0, -0.3, 0.9, -2.0], np.float32)
+    zd = np.array([-0.4, 0.8, 0.3, 1.1, -1.5, 0.2, 0.6], np.float32)
+    p = np.exp(zt.astype(np.float64)); p /= p.sum()
+    q = np.exp(zd.astype(np.float64)); q /= q.sum()
+    g = ((np.arange(M) + 0.5) / M).astype(np.float32)
+    xs, us, ur, wt = [], [], [], []
+    for x in range(V):
+        for u in g:
+            for u2 in g:
+                xs.append(x), us.append(u), ur.append(u2), wt.append(q[x] / (M * M))
+    B = len(xs)
+    target = np.empty((2 * B, V), np.float32)
+    target[0::2] = zt
+    target[1::2] = zt
+    step = step_from_arrays(target, np.tile(zd, (B, 1)), [1] * B, xs, [1.0] * B, us, ur, 1, "fp32")
+    announce(f"draw distribution B={B}")
+    got = run_verify(gpu_lib, step, row_lse=False)
+    dist = np.zeros(V)
+    np.add.at(dist, got["tokens"][:, 0], np.asarray(wt))
+    np.testing.assert_allclose(dist, p, atol=2.0 / M)
