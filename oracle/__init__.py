@@ -42,8 +42,9 @@ def _load():
     lib.oracle_next_sl.restype = i32
     lib.oracle_calibrate_sl_max.argtypes = [i32, P, i64, P, f64]
     lib.oracle_calibrate_sl_max.restype = f64
-    lib.oracle_sl_hat_spread.argtypes = [i32, P, P, P, i32, P, i32, i32, f64, f64, f64, f64, P, P, P]
-    lib.oracle_sl_hat_spread.restype = i32
+    lib.oracle_signal_spread.argtypes = [i32, P, P, P, i32, P, i32, i32, f64, f64, f64, f64, P, P, P, P, P, P,
+                                         P]
+    lib.oracle_signal_spread.restype = i32
     lib.oracle_sl_round_ties.argtypes = [i32, P, P, P, f64, i32, f64, P]
     lib.oracle_sl_round_ties.restype = i32
     _lib = lib
@@ -154,10 +155,12 @@ def calibrate_sl_max(accepted_per_step, kld_values, eps=1e-6):
     return float(lib.oracle_calibrate_sl_max(a_a.shape[0], a_p, k_a.shape[0], k_p, eps))
 
 
-def sl_hat_spread(hist, head, count, sl_max, seq_err, n_short=10, n_long=30, delta=0.85, eps=1e-6,
+def signal_spread(hist, head, count, sl_max, seq_err, n_short=10, n_long=30, delta=0.85, eps=1e-6,
                   sl_min=2.0, rho=1e-4):
-    """SL_hat and its first-order spread under a relative uncertainty ``rho`` on every
-    history entry (post-step rings)."""
+    """First-order spreads of var_short, var_long, wvir, sf and SL_hat under a relative
+    uncertainty ``rho`` on every history entry (post-step rings).  Returns a dict with
+    ``sl_hat`` and the spreads ``d_var_short``, ``d_var_long``, ``d_wvir``, ``d_sf``,
+    ``d_sl_hat``."""
     lib = _load()
     h_a, h_p = _c(hist, np.float64)
     B, W = h_a.shape
@@ -165,12 +168,19 @@ def sl_hat_spread(hist, head, count, sl_max, seq_err, n_short=10, n_long=30, del
     c_a, c_p = _c(count, np.int32)
     mx_a, mx_p = _c(sl_max, np.float64)
     e_a, e_p = _c(seq_err, np.uint32)
-    hat = np.zeros(B, np.float64)
-    dhat = np.zeros(B, np.float64)
+    out = {k: np.zeros(B, np.float64) for k in ("sl_hat", "d_sl_hat", "d_var_short", "d_var_long", "d_wvir",
+                                                 "d_sf")}
     P = lambda a: a.ctypes.data_as(ctypes.c_void_p)
-    lib.oracle_sl_hat_spread(B, h_p, hd_p, c_p, W, mx_p, n_short, n_long, delta, eps, sl_min, rho,
-                             e_p, P(hat), P(dhat))
-    return hat, dhat
+    lib.oracle_signal_spread(B, h_p, hd_p, c_p, W, mx_p, n_short, n_long, delta, eps, sl_min, rho, e_p,
+                             P(out["sl_hat"]), P(out["d_sl_hat"]), P(out["d_var_short"]), P(out["d_var_long"]),
+                             P(out["d_wvir"]), P(out["d_sf"]))
+    return out
+
+
+def sl_hat_spread(hist, head, count, sl_max, seq_err, rho=1e-4, **kw):
+    """SL_hat and its first-order spread (see ``signal_spread``)."""
+    o = signal_spread(hist, head, count, sl_max, seq_err, rho=rho, **kw)
+    return o["sl_hat"], o["d_sl_hat"]
 
 
 def sl_round_ties(hat, dhat, seq_err, sl_min=2.0, sl_hi=8, tau=1e-5):

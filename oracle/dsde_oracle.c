@@ -57,7 +57,7 @@
 #define ORC_BAD_LAYOUT 1u   /* SL_b outside [0, k_max] or cu_sl inconsistent */
 #define ORC_BAD_TOKEN 2u    /* drafted token outside [0, V) */
 #define ORC_BAD_LOGIT 4u    /* non-finite logit in a row the step uses */
-#define ORC_BAD_TEMP 8u     /* temperature not finite or not > 0 */
+#define ORC_BAD_TEMP 8u     /* temperature not finite or outside [2^-16, 2^16] */
 #define ORC_BAD_UNIFORM 16u /* uniform outside [0, 1) */
 #define ORC_BAD_SIGNAL 32u  /* non-finite signal value */
 #define ORC_BAD_STATE 64u   /* ring head/count outside their ranges */
@@ -149,7 +149,8 @@ static void verify_sequence(const verify_job *J, int32_t b) {
     float u = J->u_res[b];
     if (!(u >= 0.0f && u < 1.0f)) err |= ORC_BAD_UNIFORM;
   }
-  if (!(isfinite(T) && T > 0.0)) err |= ORC_BAD_TEMP;
+  /* the admissible temperature range of the boundary: [2^-16, 2^16] */
+  if (!(T >= ldexp(1.0, -16) && T <= ldexp(1.0, 16))) err |= ORC_BAD_TEMP;
   if (!err) {
     for (int32_t j = 0; j < SL; ++j)
       if (!row_is_finite(J->target, J->dtype, V, trow0 + j) ||
@@ -209,10 +210,12 @@ static void verify_sequence(const verify_job *J, int32_t b) {
   } else {
     tr = trow0 + SL;
     if (!row_is_finite(J->target, J->dtype, V, tr)) {
+      /* a non-finite bonus row withholds the token only: the KLD of the
+       * drafted pairs stays defined */
       free(lse_p);
       free(lse_q);
-      err |= ORC_BAD_LOGIT;
-      goto fail;
+      J->seq_err[b] = ORC_BAD_LOGIT;
+      return;
     }
     lp_row = row_lse(J->target, J->dtype, V, tr, T);
   }
@@ -471,42 +474,55 @@ double oracle_calibrate_sl_max(int32_t n_steps, const int32_t *accepted_per_step
 /* tie analysis of SL decisions                                        */
 /* ------------------------------------------------------------------ */
 
-/* Spread of SL_hat under a relative uncertainty rho on every history entry a
- * sequence uses (including the one pushed this step, which is also the
- * mu_KLD,last of SF).  For each entry alone the SL rule is re-evaluated with
- * the entry scaled by (1 - rho) and (1 + rho); the larger change is kept and the
- * changes are summed over entries (a first-order bound).  Eq. 8 is continuous
- * at SF * WVIR = 1, so only SL_hat's value matters to the decision.
- * Inputs are the post-step rings and sl_max; outputs SL_hat and its spread. */
-int oracle_sl_hat_spread(int32_t B, const double *hist, const int32_t *head, const int32_t *count, int32_t W,
+/* First-order spread of the signal outputs under a relative uncertainty rho
+ * on every history entry a sequence uses (including the one pushed this step,
+ * which is also the mu_KLD,last of SF).  For each entry alone the signal is
+ * re-evaluated with the entry scaled by (1 - rho) and (1 + rho); per output the
+ * larger change is kept and the changes are summed over entries.  Inputs are
+ * the post-step rings and sl_max; every output pointer may be NULL.  Eq. 8 is
+ * continuous at SF * WVIR = 1, so SL_hat's spread bounds its decision. */
+int oracle_signal_spread(int32_t B, const double *hist, const int32_t *head, const int32_t *count, int32_t W,
                          const double *sl_max, int32_t n_short, int32_t n_long, double delta, double eps,
-                         double sl_min, double rho, const uint32_t *seq_err, double *hat, double *dhat) {
+                         double sl_min, double rho, const uint32_t *seq_err, double *hat, double *dhat,
+                         double *dvar_s, double *dvar_l, double *dwvir, double *dsf) {
   double *h = (double *)malloc(sizeof(double) * (size_t)(W > 0 ? W : 1));
   for (int32_t b = 0; b < B; ++b) {
-    hat[b] = NAN;
-    dhat[b] = NAN;
-    if (seq_err[b]) continue;
-    const int32_t cnt = count[b];
-    for (int32_t i = 1; i <= cnt; ++i) h[i - 1] = hist[(int64_t)b * W + ((head[b] - i) % W + W) % W];
-    double vs, vl, wv, sf;
-    signal_from_history(h, cnt, cnt > 0 ? h[0] : 0.0, n_short, n_long, delta, eps, &vs, &vl, &wv, &sf);
-    hat[b] = sl_hat_of(sf, wv, sl_max[b], sl_min);
-    double spread = 0.0;
-    const int32_t nuse = n_long < cnt ? n_long : cnt;
-    for (int32_t i = 0; i < nuse; ++i) {
-      const double keep = h[i];
-      double worst = 0.0;
-      for (int sgn = -1; sgn <= 1; sgn += 2) {
-        h[i] = keep * (1.0 + sgn * rho);
-        double vs2, vl2, wv2, sf2;
-        signal_from_history(h, cnt, h[0], n_short, n_long, delta, eps, &vs2, &vl2, &wv2, &sf2);
-        double d = fabs(sl_hat_of(sf2, wv2, sl_max[b], sl_min) - hat[b]);
-        if (d > worst) worst = d;
+    double base[5] = {NAN, NAN, NAN, NAN, NAN}, spread[5] = {NAN, NAN, NAN, NAN, NAN};
+    if (!seq_err[b]) {
+      const int32_t cnt = count[b];
+      for (int32_t i = 1; i <= cnt; ++i) h[i - 1] = hist[(int64_t)b * W + ((head[b] - i) % W + W) % W];
+      double vs, vl, wv, sf;
+      signal_from_history(h, cnt, cnt > 0 ? h[0] : 0.0, n_short, n_long, delta, eps, &vs, &vl, &wv, &sf);
+      base[0] = vs;
+      base[1] = vl;
+      base[2] = wv;
+      base[3] = sf;
+      base[4] = sl_hat_of(sf, wv, sl_max[b], sl_min);
+      for (int k = 0; k < 5; ++k) spread[k] = 0.0;
+      const int32_t nuse = n_long < cnt ? n_long : cnt;
+      for (int32_t i = 0; i < nuse; ++i) {
+        const double keep = h[i];
+        double worst[5] = {0.0, 0.0, 0.0, 0.0, 0.0};
+        for (int sgn = -1; sgn <= 1; sgn += 2) {
+          h[i] = keep * (1.0 + sgn * rho);
+          double vs2, vl2, wv2, sf2;
+          signal_from_history(h, cnt, h[0], n_short, n_long, delta, eps, &vs2, &vl2, &wv2, &sf2);
+          const double now[5] = {vs2, vl2, wv2, sf2, sl_hat_of(sf2, wv2, sl_max[b], sl_min)};
+          for (int k = 0; k < 5; ++k) {
+            double d = fabs(now[k] - base[k]);
+            if (d > worst[k]) worst[k] = d;
+          }
+        }
+        h[i] = keep;
+        for (int k = 0; k < 5; ++k) spread[k] += worst[k];
       }
-      h[i] = keep;
-      spread += worst;
     }
-    dhat[b] = spread;
+    if (dvar_s) dvar_s[b] = spread[0];
+    if (dvar_l) dvar_l[b] = spread[1];
+    if (dwvir) dwvir[b] = spread[2];
+    if (dsf) dsf[b] = spread[3];
+    if (hat) hat[b] = base[4];
+    if (dhat) dhat[b] = spread[4];
   }
   free(h);
   return 0;

@@ -283,7 +283,9 @@ def test_error_bits_and_fallback_outputs(orc):
                                      orc.BAD_LOGIT]
     for b in range(1, 6):
         assert out["accepted"][b] == 0 and (out["tokens"][b] == -1).all()
-        assert np.isnan(out["kld"][2 * b: 2 * b + 2]).all()
+    assert np.isnan(out["kld"][2:10]).all()
+    # a non-finite bonus row withholds only the token
+    assert np.isfinite(out["kld"][10:12]).all() and np.isfinite(out["kld"][:2]).all()
     # a bad bonus row of a sequence that rejects early is never read
     kw2 = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in base.items()}
     kw2["u_acc"][0] = U_MAX
@@ -297,6 +299,10 @@ def test_error_bits_and_fallback_outputs(orc):
     kw3["cu_sl"] = base["cu_sl"].copy()
     kw3["cu_sl"][3] += 1
     assert (orc.verify(**kw3)["seq_err"] == orc.BAD_LAYOUT).all()
+    # temperatures outside [2^-16, 2^16]
+    kw4 = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in base.items()}
+    kw4["temperature"][:4] = [2.0 ** -17, 2.0 ** -16, 2.0 ** 16, 2.0 ** 17]
+    assert list(orc.verify(**kw4)["seq_err"][:4]) == [orc.BAD_TEMP, 0, 0, orc.BAD_TEMP]
 
 
 # ---------------------------------------------------------------- KLD signal
