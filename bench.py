@@ -1,9 +1,11 @@
 #!/usr/bin/env python3
 """Benchmark of the DSDE verification step on one MI355X.
 
-One step = dsde_verify + dsde_kld_signal + dsde_next_sl over one batch of
-synthetic inputs already resident in HBM (workload b256 by default: B=256,
-SL ~ U{1..8}, V=128256 bf16, T = 0.7 / 1.0 alternating).  Two input copies
+One step = verification + KLD signal update + SL rule with the batch cap
+(dsde_step, which is bit-identical to dsde_verify, dsde_kld_signal and
+dsde_next_sl in sequence) over one batch of synthetic inputs already resident
+in HBM (workload b256 by default: B=256, SL ~ U{1..8}, V=128256 bf16,
+T = 0.7 / 1.0 alternating).  Two input copies
 alternate between steps so that no step finds its logits in the 256 MB
 last-level cache.
 
@@ -64,46 +66,48 @@ def main():
     esz = 2 if s0.target.dtype == torch.bfloat16 else 4
     ws = dsde.new_workspace(B, N, V, k_max, device=dev)
     outs = [None, None]
-    sig_out = None
-    nsl_out = None
 
     def one_step(i):
-        nonlocal sig_out, nsl_out
         s = copies[i % 2]
-        outs[i % 2] = dsde.verify(s.target, s.draft, s.sl, s.cu_sl, s.draft_tokens, s.temperature, s.u_acc,
-                                  s.u_res, k_max, out=outs[i % 2], workspace=ws)
-        sig_out = dsde.kld_signal(s.sl, s.cu_sl, outs[i % 2]["kld"], st.hist, st.head, st.count, out=sig_out)
-        nsl_out = dsde.next_sl(sig_out["sf"], sig_out["wvir"], st.sl_max, 2.0, k_max, out=nsl_out)
+        outs[i % 2] = dsde.step(s.target, s.draft, s.sl, s.cu_sl, s.draft_tokens, s.temperature, s.u_acc, s.u_res,
+                                k_max, st.hist, st.head, st.count, st.sl_max, out=outs[i % 2], workspace=ws)
 
     for i in range(args.warmup):
         one_step(i)
     torch.cuda.synchronize()
-
-    # per-step HIP events around the row-statistics kernel, recorded by the library
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     stream = torch.cuda.current_stream()
-    for a, b in ev:  # materialise the underlying events
-        a.record(stream)
-        b.record(stream)
-    torch.cuda.synchronize()
-    step_ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
 
+    # timed region: K whole steps between two events on the launch stream
+    step_ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     step_ev[0].record(stream)
     for i in range(args.steps):
-        dsde.set_profile_events(*ev[i])
         one_step(args.warmup + i)
     step_ev[1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+
+    # second timed region of K steps with HIP events the library records around
+    # the row-statistics kernel of each step (kept out of the first region:
+    # each event record costs a few microseconds of stream time)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a_, b_ in ev:  # materialise the underlying events
+        a_.record(stream)
+        b_.record(stream)
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        dsde.set_profile_events(*ev[i])
+        one_step(args.warmup + args.steps + i)
+    torch.cuda.synchronize()
     dsde.set_profile_events(None, None)
 
     gpu_ms = step_ev[0].elapsed_time(step_ev[1])
     ms_per_step = gpu_ms / args.steps
     k1_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     rows = 2 * N + B
-    acc = outs[(args.warmup + args.steps - 1) % 2]["accepted"].cpu().numpy()
+    last = (args.warmup + 2 * args.steps - 1) % 2
+    acc = outs[last]["accepted"].cpu().numpy()
     sls = s0.sl.cpu().numpy()
     b_full = int((acc == sls).sum())
     io_bytes = 4 * (3 * N + 2 * B + B * (k_max + 1)) + 8 * B * cfg["W"]
@@ -137,16 +141,14 @@ def main():
         "hbm_frac_algorithmic": alg_bytes / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBPS,
         "wall_ms_per_step": wall * 1e3 / args.steps,
         "b_full": b_full,
-        "roofline": {"bound": "hbm", "kernel": "pair_stats_kernel", "achieved": k1_gbps, "peak": PEAK_HBM_GBPS,
+        "roofline": {"bound": "hbm", "kernel": "stats_kernel_bf16", "achieved": k1_gbps, "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": k1_gbps / PEAK_HBM_GBPS, "traffic": traffic,
                      "kernel_ms": k1_ms, "algorithmic_bytes": k1_bytes},
         "cpu_baseline": None,
     }
 
     if not args.no_cpu_baseline:
-        result["cpu_baseline"], result["parity"] = cpu_baseline(copies[(args.warmup + args.steps - 1) % 2],
-                                                                outs[(args.warmup + args.steps - 1) % 2],
-                                                                args.cpu_seconds)
+        result["cpu_baseline"], result["parity"] = cpu_baseline(copies[last], outs[last], st, args.cpu_seconds)
     if args.copy_calibration:
         n = 1 << 30
         src = torch.empty(n, dtype=torch.uint8, device=dev)
@@ -167,20 +169,27 @@ def kernel_hash():
     return h.hexdigest()[:16]
 
 
-def cpu_baseline(step, out, seconds):
-    """The oracle, as it stands, on the host: whole steps repeated until about
-    ``seconds`` of CPU time have passed; also checks the GPU step against it."""
+def cpu_baseline(step, out, st, seconds):
+    """The oracle, as it stands, on the host: whole steps (verify, signal update,
+    SL rule) repeated until about ``seconds`` of CPU time have passed; also checks
+    the GPU's last step against it."""
     import numpy as np
 
     import oracle
     import workloads as W
     host = W.host_arrays(step)
+    hist = st.hist.cpu().numpy()
+    head = st.head.cpu().numpy()
+    count = st.count.cpu().numpy()
+    smax = st.sl_max.cpu().numpy().astype(np.float64)
     threads = min(16, os.cpu_count() or 1)
     t0 = time.perf_counter()
     n = 0
     ref = None
     while True:
         ref = oracle.verify(**host, n_threads=threads)
+        sig = oracle.kld_signal(host["sl"], host["cu_sl"], ref["kld"], hist, head, count)
+        oracle.next_sl(sig["sf"], sig["wvir"], smax, 2.0, step.k_max)
         n += 1
         if time.perf_counter() - t0 >= seconds or n >= 20:
             break
@@ -192,13 +201,14 @@ def cpu_baseline(step, out, seconds):
     ok = (ref["seq_err"] == 0) & (ref["acc_tie"] == 0) & (ref["cdf_tie"] == 0)
     mism = int((ok & ((acc != ref["accepted"]) | (tok != ref["tokens"]).any(axis=1))).sum())
     kg = out["kld"].cpu().numpy().astype(np.float64)
-    kerr = float(np.max(np.abs(kg - ref["kld"]) / np.maximum(np.abs(ref["kld"]), 1e-12)))
+    fine = np.repeat(ref["seq_err"] == 0, host["sl"])
+    kerr = float(np.max((np.abs(kg - ref["kld"]) / (1e-4 * np.abs(ref["kld"]) + 1e-6))[fine])) if fine.any() else 0.0
     cpu = {"value": rows / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
-           "sample": f"the full timed step (B={len(host['sl'])}, {rows} logit rows, V={host['V']}), "
-                     f"{n} repetition(s), {threads} threads, fp64",
+           "sample": f"the full step (verify + signal + SL rule; B={len(host['sl'])}, {rows} logit rows, "
+                     f"V={host['V']}), {n} repetition(s), {threads} threads, fp64",
            "seconds_per_step": dt}
     parity = {"compared": int(ok.sum()), "ties": int((ref["acc_tie"] | ref["cdf_tie"]).sum()),
-              "mismatches": mism, "kld_max_rel_err": kerr}
+              "mismatches": mism, "kld_err_over_tolerance": kerr}
     return cpu, parity
 
 

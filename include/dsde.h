@@ -28,9 +28,15 @@
  *     DSDE_INVALID_ARG or DSDE_WORKSPACE_TOO_SMALL; nothing is enqueued then.
  *     DSDE_DEVICE_ERROR reports a failed kernel launch.
  *   - Data errors found on the device are reported per sequence in seq_err[b]
- *     (bits DSDE_ERR_*).  A flagged sequence gets defined outputs: accepted = 0,
- *     every token = pad_id, kld = NaN at its positions (not written when the
- *     layout itself is invalid), NaN signal values, and it is left out of the cap.
+ *     (bits DSDE_ERR_*).  A flagged sequence gets defined outputs: accepted = 0
+ *     and every token = pad_id; kld = NaN at its positions when its drafted
+ *     pairs could not be evaluated (a bad token, temperature, uniform or a
+ *     non-finite logit in a drafted pair; not written when the layout itself is
+ *     invalid).  A non-finite bonus row only withholds the token: the KLD values
+ *     stay.  NaN KLD makes the signal NaN, and such sequences are left out of
+ *     the cap.
+ *   - Finite logits are assumed to satisfy |z| <= 2^64 (any real logit does);
+ *     larger magnitudes are outside the contract.
  *
  * Packed ragged layout (no padding rows): with N = sum_b SL_b and
  * cu_sl[b] = SL_0 + ... + SL_{b-1} (cu_sl[0] = 0, cu_sl[B] = N),
@@ -67,7 +73,7 @@ extern "C" {
 #define DSDE_ERR_TOKEN 2u    /* a drafted token outside [0, V) */
 #define DSDE_ERR_LOGIT 4u    /* NaN or +-inf in a row the step reads (every drafted pair; the bonus row
                                 only when it is sampled) */
-#define DSDE_ERR_TEMP 8u     /* temperature not finite or not > 0 */
+#define DSDE_ERR_TEMP 8u     /* temperature not finite or outside [2^-16, 2^16] */
 #define DSDE_ERR_UNIFORM 16u /* a uniform outside [0, 1) */
 #define DSDE_ERR_SIGNAL 32u  /* non-finite KLD, SF, WVIR or SL_max, or SL_max < sl_min */
 #define DSDE_ERR_STATE 64u   /* ring head outside [0, W) or count outside [0, W] */
@@ -98,7 +104,7 @@ size_t dsde_verify_workspace_bytes(int32_t B, int64_t N, int64_t V, int32_t k_ma
  *                                        0 <= k_max <= DSDE_MAX_K)
  *   sl [B], cu_sl [B+1]     int32       per-sequence SL and its exclusive prefix sums
  *   draft_tokens [N]        int32       the drafted token at each position
- *   temperature [B]         float       per-sequence sampling temperature T_b (> 0);
+ *   temperature [B]         float       per-sequence sampling temperature T_b in [2^-16, 2^16];
  *                                       p = softmax(z_target / T_b), q = softmax(z_draft / T_b)
  *   u_acc [N]               float       acceptance uniforms in [0, 1), one per position
  *   u_res [B]               float       draw uniforms in [0, 1), one per sequence
@@ -172,10 +178,28 @@ int32_t dsde_next_sl(int32_t B, const float *sf, const float *wvir, const float 
                      void *stream);
 
 /*
+ * The whole step fused: dsde_verify, then dsde_kld_signal on the KLD it
+ * produces, then dsde_next_sl on the signal it produces, with the arguments
+ * of those three calls (see them for meaning and layout), in four kernel
+ * launches instead of six.  Outputs are bit-identical to the three calls made
+ * in sequence; seq_err is the OR of their error bits, except that a layout
+ * error (DSDE_ERR_LAYOUT) also skips the signal update.
+ * For serving loops that run the complete verification step.
+ */
+int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
+                  int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
+                  const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
+                  int32_t *accepted, int32_t *tokens, float *kld, double *row_lse, float *hist, int32_t *head,
+                  int32_t *count, int32_t W, int32_t n_short, int32_t n_long, float delta, float eps,
+                  float *mu_last, float *var_short, float *var_long, float *wvir, float *sf, const float *sl_max,
+                  float sl_min, int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
+                  void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Profiling hook: when both events are non-NULL (hipEvent_t), every later
- * dsde_verify records `start` just before and `stop` just after its row
- * statistics kernel (the pass that reads every drafted row pair once) on its
- * stream.  Passing NULLs turns it off.  Process-wide; not thread-safe.
+ * dsde_verify or dsde_step records `start` just before and `stop` just after
+ * its row statistics kernel (the pass that reads every drafted row pair once)
+ * on its stream.  Passing NULLs turns it off.  Process-wide; not thread-safe.
  */
 int32_t dsde_set_profile_events(void *start, void *stop);
 

@@ -19,7 +19,7 @@ FP32, BF16 = 0, 1
 ERR_LAYOUT, ERR_TOKEN, ERR_LOGIT, ERR_TEMP, ERR_UNIFORM, ERR_SIGNAL, ERR_STATE = 1, 2, 4, 8, 16, 32, 64
 MAX_K = 63
 EXPORTS = ("dsde_abi_version", "dsde_status_string", "dsde_verify_workspace_bytes", "dsde_verify",
-           "dsde_kld_signal", "dsde_next_sl", "dsde_set_profile_events")
+           "dsde_step", "dsde_kld_signal", "dsde_next_sl", "dsde_set_profile_events")
 
 _lib = None
 
@@ -46,6 +46,10 @@ def load(path: str = LIB_PATH):
     lib.dsde_verify_workspace_bytes.argtypes = [i32, i64, i64, i32]
     lib.dsde_verify.restype = i32
     lib.dsde_verify.argtypes = [P, P, i32, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P, P, P, sz, P]
+    lib.dsde_step.restype = i32
+    lib.dsde_step.argtypes = [P, P, i32, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P,
+                              P, P, P, i32, i32, i32, f32, f32, P, P, P, P, P,
+                              P, f32, i32, P, P, P, P, P, sz, P]
     lib.dsde_kld_signal.restype = i32
     lib.dsde_kld_signal.argtypes = [i32, i64, P, P, P, P, P, P, i32, i32, i32, f32, f32, P, P, P, P, P, P, P]
     lib.dsde_next_sl.restype = i32
@@ -96,12 +100,7 @@ def verify(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_
     """``dsde_verify`` on torch tensors.  Returns (accepted, tokens, kld, seq_err);
     pass ``out`` (a dict with those keys) to reuse output buffers."""
     lib = load()
-    if target.dtype == torch.bfloat16:
-        dt = BF16
-    elif target.dtype == torch.float32:
-        dt = FP32
-    else:
-        raise DsdeError("logits must be bfloat16 or float32")
+    dt = _logits_dtype(target)
     V = int(target.shape[1])
     B = int(sl.shape[0])
     N = int(draft.shape[0]) if draft is not None else 0
@@ -130,6 +129,62 @@ def verify(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_
         _ptr(out["seq_err"], None, B, "seq_err"),
         _ptr(row_lse, torch.float64, 2 * N, "row_lse") if row_lse is not None else None,
         _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc)
+    return out
+
+
+def _logits_dtype(target):
+    if target.dtype == torch.bfloat16:
+        return BF16
+    if target.dtype == torch.float32:
+        return FP32
+    raise DsdeError("logits must be bfloat16 or float32")
+
+
+def step(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, hist, head, count,
+         sl_max, n_short=10, n_long=30, delta=0.85, eps=1e-6, sl_min=2.0, sl_hi=None, pad_id=-1,
+         out=None, workspace=None, row_lse=None, stream=None):
+    """``dsde_step``: verify + signal update + SL rule in one call.  hist/head/count are
+    updated in place; returns a dict of every output (accepted, tokens, kld, mu_last,
+    var_short, var_long, wvir, sf, sl_hat, sl_cap, sl_next, seq_err)."""
+    lib = load()
+    dt = _logits_dtype(target)
+    V = int(target.shape[1])
+    B = int(sl.shape[0])
+    N = int(draft.shape[0]) if draft is not None else 0
+    W = int(hist.shape[1])
+    sl_hi = k_max if sl_hi is None else sl_hi
+    dev = target.device
+    if int(target.shape[0]) != N + B:
+        raise DsdeError(f"target has {target.shape[0]} rows, expected N + B = {N + B}")
+    if out is None:
+        out = {"accepted": torch.empty(B, dtype=torch.int32, device=dev),
+               "tokens": torch.empty((B, k_max + 1), dtype=torch.int32, device=dev),
+               "kld": torch.empty(max(N, 1), dtype=torch.float32, device=dev)[:N],
+               "seq_err": torch.empty(B, dtype=torch.int32, device=dev),
+               "sl_cap": torch.empty(1, dtype=torch.float32, device=dev),
+               "sl_next": torch.empty(B, dtype=torch.int32, device=dev)}
+        for k in ("mu_last", "var_short", "var_long", "wvir", "sf", "sl_hat"):
+            out[k] = torch.empty(B, dtype=torch.float32, device=dev)
+    if workspace is None:
+        workspace = new_workspace(B, N, V, k_max, device=dev)
+    f32 = torch.float32
+    rc = lib.dsde_step(
+        _ptr(target, name="target"), _ptr(draft, name="draft") if N > 0 else None, dt, V, B, N, k_max,
+        _ptr(sl, torch.int32, B, "sl"), _ptr(cu_sl, torch.int32, B + 1, "cu_sl"),
+        _ptr(draft_tokens, torch.int32, N, "draft_tokens") if N > 0 else None,
+        _ptr(temperature, f32, B, "temperature"), _ptr(u_acc, f32, N, "u_acc") if N > 0 else None,
+        _ptr(u_res, f32, B, "u_res"), int(pad_id),
+        _ptr(out["accepted"], torch.int32, B), _ptr(out["tokens"], torch.int32, B * (k_max + 1)),
+        _ptr(out["kld"], f32, N) if N > 0 else None,
+        _ptr(row_lse, torch.float64, 2 * N, "row_lse") if row_lse is not None else None,
+        _ptr(hist, f32, B * W, "hist"), _ptr(head, torch.int32, B, "head"), _ptr(count, torch.int32, B, "count"),
+        W, n_short, n_long, float(delta), float(eps),
+        _ptr(out["mu_last"], f32, B), _ptr(out["var_short"], f32, B), _ptr(out["var_long"], f32, B),
+        _ptr(out["wvir"], f32, B), _ptr(out["sf"], f32, B), _ptr(sl_max, f32, B, "sl_max"), float(sl_min),
+        int(sl_hi), _ptr(out["sl_hat"], f32, B), _ptr(out["sl_cap"], f32, 1), _ptr(out["sl_next"], torch.int32, B),
+        _ptr(out["seq_err"], None, B), _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
+        _stream(stream))
     _check(rc)
     return out
 

@@ -81,6 +81,76 @@ int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t
   a.stream = static_cast<hipStream_t>(stream);
   a.prof_start = g_prof_start;
   a.prof_stop = g_prof_stop;
+  a.signal = nullptr;
+  return dsde::launch_verify(a);
+}
+
+int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
+                  int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
+                  const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
+                  int32_t *accepted, int32_t *tokens, float *kld, double *row_lse, float *hist, int32_t *head,
+                  int32_t *count, int32_t W, int32_t n_short, int32_t n_long, float delta, float eps,
+                  float *mu_last, float *var_short, float *var_long, float *wvir, float *sf, const float *sl_max,
+                  float sl_min, int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
+                  void *workspace, size_t workspace_bytes, void *stream) {
+  if (dtype != DSDE_FP32 && dtype != DSDE_BF16) return DSDE_INVALID_ARG;
+  if (!verify_sizes_ok(B, N, V, k_max)) return DSDE_INVALID_ARG;
+  if (!target_logits || !sl || !cu_sl || !temperature || !u_res || !accepted || !tokens || !seq_err ||
+      !workspace)
+    return DSDE_INVALID_ARG;
+  if (N > 0 && (!draft_logits || !draft_tokens || !u_acc || !kld)) return DSDE_INVALID_ARG;
+  if (W < 1 || n_short < 1 || n_short > n_long) return DSDE_INVALID_ARG;
+  if (!(delta > 0.0f && delta <= 1.0f) || !(eps >= 0.0f) || !isfinite(eps)) return DSDE_INVALID_ARG;
+  if (!hist || !head || !count || !mu_last || !var_short || !var_long || !wvir || !sf) return DSDE_INVALID_ARG;
+  if (!isfinite(sl_min) || ceilf(sl_min) > float(sl_hi)) return DSDE_INVALID_ARG;
+  if (!sl_max || !sl_hat || !sl_cap || !sl_next) return DSDE_INVALID_ARG;
+  if (workspace_bytes < dsde::workspace_layout(B, N, V).total) return DSDE_WORKSPACE_TOO_SMALL;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return DSDE_INVALID_ARG;
+  dsde::SignalArgs sg;
+  sg.hist = hist;
+  sg.head = head;
+  sg.count = count;
+  sg.W = W;
+  sg.n_short = n_short;
+  sg.n_long = n_long;
+  sg.delta = delta;
+  sg.eps = eps;
+  sg.mu_last = mu_last;
+  sg.var_short = var_short;
+  sg.var_long = var_long;
+  sg.wvir = wvir;
+  sg.sf = sf;
+  sg.sl_max = sl_max;
+  sg.sl_min = sl_min;
+  sg.sl_hi = sl_hi;
+  sg.sl_hat = sl_hat;
+  sg.sl_cap = sl_cap;
+  sg.sl_next = sl_next;
+  dsde::VerifyArgs a;
+  a.target = target_logits;
+  a.draft = draft_logits;
+  a.dtype = dtype;
+  a.V = V;
+  a.B = B;
+  a.N = N;
+  a.k_max = k_max;
+  a.sl = sl;
+  a.cu_sl = cu_sl;
+  a.draft_tokens = draft_tokens;
+  a.temperature = temperature;
+  a.u_acc = u_acc;
+  a.u_res = u_res;
+  a.pad_id = pad_id;
+  a.accepted = accepted;
+  a.tokens = tokens;
+  a.kld = kld;
+  a.seq_err = seq_err;
+  a.row_lse = row_lse;
+  a.workspace = workspace;
+  a.stream = static_cast<hipStream_t>(stream);
+  a.prof_start = g_prof_start;
+  a.prof_stop = g_prof_stop;
+  a.signal = &sg;
   return dsde::launch_verify(a);
 }
 

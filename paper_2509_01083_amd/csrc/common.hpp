@@ -14,29 +14,39 @@ constexpr int kEltsPerThread = 32;         // logits per row per thread in one c
 constexpr int kChunk = kThreads * kEltsPerThread;  // logits per row chunk (8192)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr double kLn2 = 0.6931471805599453;
+// Temperatures outside [2^-16, 2^16] are rejected so that every scaled logit
+// z * log2(e) / T of a finite logit with |z| <= 2^64 stays far inside fp32.
+constexpr float kMinTemp = 1.52587890625e-05f, kMaxTemp = 65536.0f;
 
-// Per drafted position, written by the set-up kernel: the target row of the
-// pair (-1 when its sequence is flagged) and the log2-domain scale
-// c = log2(e) / T_b as raw float bits.
-struct PairInfo {
+// One row pair of the statistics pass, in processing order: the drafted
+// position (pair index), its target row (-1 when the layout is invalid) and
+// the log2-domain scale c = log2(e) / T_b as raw float bits.
+struct WorkItem {
+  int32_t pair;
   int32_t target_row;
-  int32_t scale_bits;
+  uint32_t scale_bits;
+  int32_t pad;
 };
 
-// Row statistics of one chunk of one drafted row pair.  Every sum is taken
-// relative to the chunk's own reference shifts mt, md (log2 domain):
-//   sp = sum 2^(z_t c - mt),   sq = sum 2^(z_d c - md),
+// Row statistics of one chunk of one drafted row pair, relative to the
+// chunk's reference shifts mt, md (log2 domain):
+//   sp = sum 2^(z_t c - mt),  sq = sum 2^(z_d c - md),
 //   a  = sum 2^(z_t c - mt) * ((z_t c - mt) - (z_d c - md)).
 struct alignas(16) PairChunk {
   float mt, md;
-  float pad0, pad1;
   double sp, sq, a;
-  double pad2;
 };
 
-// What the draw of one sequence needs, written by the acceptance kernel.
+// The target and draft logits at the drafted token, captured by the chunk
+// that holds it.
+struct Gathered {
+  float zt, zd;
+};
+
+// What the draw of one sequence needs, written by the chunk-0 workgroup of
+// the draw-chunk kernel.
 struct alignas(16) DrawJob {
-  int32_t kind;        // 0: residual of a rejected pair, 1: bonus row, -1: nothing (flagged)
+  int32_t kind;        // 0: residual of the first rejected pair, 1: bonus row, -1: nothing (flagged)
   int32_t accepted;    // a_b
   int32_t target_row;
   int32_t draft_row;   // -1 for the bonus row
@@ -51,26 +61,31 @@ struct alignas(16) DrawJob {
 // fallback p; bonus: e = 2^(z c - ref) relative to the chunk reference.
 struct alignas(16) DrawChunk {
   double w;
-  double p;    // residual: sum of p over the chunk (used when the residual mass is 0)
-  float ref;   // bonus: chunk reference shift
-  int32_t bad; // bonus: a NaN or +-inf logit was seen
+  double p;
+  float ref;
+  int32_t bad;  // bonus: a NaN or +-inf logit was seen
   int32_t pad0, pad1;
 };
 
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct WorkspaceLayout {
-  size_t pair_info, pair_chunk, draw_job, draw_chunk, total;
+  size_t work, pair_chunk, gathered, draw_job, draw_chunk, total;
 };
 
+inline int64_t num_chunks(int64_t V) { return (V + kChunk - 1) / kChunk; }
+
 inline WorkspaceLayout workspace_layout(int32_t B, int64_t N, int64_t V) {
-  const int64_t nc = (V + kChunk - 1) / kChunk;
+  const int64_t nc = num_chunks(V);
+  const size_t n = size_t(N > 0 ? N : 1);
   WorkspaceLayout L;
   size_t off = 0;
-  L.pair_info = off;
-  off += align_up(sizeof(PairInfo) * size_t(N > 0 ? N : 1));
+  L.work = off;
+  off += align_up(sizeof(WorkItem) * n);
   L.pair_chunk = off;
-  off += align_up(sizeof(PairChunk) * size_t(N > 0 ? N : 1) * size_t(nc));
+  off += align_up(sizeof(PairChunk) * n * size_t(nc));
+  L.gathered = off;
+  off += align_up(sizeof(Gathered) * n);
   L.draw_job = off;
   off += align_up(sizeof(DrawJob) * size_t(B));
   L.draw_chunk = off;
@@ -78,6 +93,21 @@ inline WorkspaceLayout workspace_layout(int32_t B, int64_t N, int64_t V) {
   L.total = off;
   return L;
 }
+
+// Arguments of the signal update and the SL rule when they run fused behind
+// the verification (dsde_step).
+struct SignalArgs {
+  float *hist;
+  int32_t *head, *count;
+  int32_t W, n_short, n_long;
+  float delta, eps;
+  float *mu_last, *var_short, *var_long, *wvir, *sf;
+  const float *sl_max;
+  float sl_min;
+  int32_t sl_hi;
+  float *sl_hat, *sl_cap;
+  int32_t *sl_next;
+};
 
 struct VerifyArgs {
   const void *target, *draft;
@@ -96,6 +126,7 @@ struct VerifyArgs {
   void *workspace;
   hipStream_t stream;
   hipEvent_t prof_start, prof_stop;
+  const SignalArgs *signal;  // non-null: fused signal update and SL rule
 };
 
 int launch_verify(const VerifyArgs &a);

@@ -1,34 +1,45 @@
 // Batched speculative verification with ragged per-sequence speculation
 // lengths on gfx950: row statistics + per-token KLD, acceptance scan, and the
-// inverse-CDF draw from the residual max(0, p - q) or the bonus row.
+// inverse-CDF draw from the residual max(0, p - q) or the bonus row
+// (speculative sampling, Sec. 2.1; ragged layout, bonus and pad, Sec. 3.2;
+// per-token KLD of the SL adapter, Sec. 3.1.2).
 //
 // Kernels, in launch order on the caller's stream:
-//   setup_kernel        one workgroup: validates the packed layout and the
-//                       per-sequence inputs, writes seq_err and the per-pair
-//                       (target row, scale) table.
-//   pair_stats_kernel   one workgroup per (drafted pair, 8192-logit chunk):
-//                       reads the chunk of the target and the draft row once
-//                       and writes the chunk's max-shifted exponential sums of
-//                       p and q and the KL accumulator.  Carries almost all HBM
-//                       bytes of the step; bound by HBM bandwidth.
-//   accept_kernel       one wavefront per sequence, one lane per drafted
-//                       position: combines the chunk partials (fp64), writes
-//                       the KLD, evaluates u < p(x)/q(x) for every position in
-//                       fp64, and finds the first rejection with a ballot.
-//   draw_chunk_kernel   one workgroup per (sequence, chunk) of the row the draw
-//                       uses: chunk totals of max(0, p - q) (re-reading the
-//                       rejected pair) or of the bonus row's exponentials.
-//   draw_kernel         one workgroup per sequence: prefix over the chunk
-//                       totals (fp64), then an ordered scan inside the one chunk
-//                       that holds u' * Z.
+//   setup_kernel       one workgroup: validates the packed layout and writes
+//                      the work list of the statistics pass (target row and
+//                      scale of every drafted pair, in sequence order).
+//   stats_kernel       one workgroup per (row pair, 8192-logit chunk): reads
+//                      the chunk of the target and draft rows once and writes
+//                      max-shifted exponential sums of p and q and the KL
+//                      accumulator; also captures the two logits at the drafted
+//                      token.  Carries almost all HBM bytes of the step.
+//   accept_kernel      one workgroup per sequence: per-sequence input checks,
+//                      the chunk partials of every drafted pair combined by
+//                      groups of lanes (fp64), the KLD, u < p(x)/q(x) for every
+//                      drafted position (fp64) and the first rejection; writes
+//                      the draw job.  Fused: the signal update of the sequence.
+//   draw_chunk_kernel  one workgroup per (sequence, chunk): the chunk's total of
+//                      the draw weights, max(0, p - q) of the rejected pair or
+//                      the bonus row's exponentials.
+//   finish_kernel      one workgroup per sequence: prefix over the chunk totals
+//                      (fp64), then an ordered scan inside the one chunk that
+//                      holds u' * Z.  Fused: one extra workgroup computes the
+//                      batch cap and the next speculation lengths.
 //
-// All reductions run in a fixed order, so results are bitwise reproducible.
+// Every reduction runs in a fixed order, so results are bitwise reproducible.
 #include <math.h>
 
 #include "common.hpp"
+#include "signal_device.hpp"
 
 namespace dsde {
 namespace {
+
+// bf16 -2^96: padding for logits past V.  It is below every admissible logit
+// (|z| <= 2^64), its exponential is exactly 0, and differences of two padding
+// values stay finite, so padding adds exactly nothing to any sum.
+constexpr uint32_t kPadBf16x2 = 0xef80ef80u;
+constexpr float kPadF32 = -7.9228162514264337593543950336e28f;  // -2^96
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -52,92 +63,6 @@ __device__ __forceinline__ float load_logit(const void *base, int dtype, int64_t
   return ((const float *)base)[idx];
 }
 
-// One row chunk held in registers: z[0..n) are the chunk's logits owned by
-// this thread, the rest are -inf.  Element i of the thread lives at
-//   VEC bf16 : 8 * (chunk*1024 + (i/8)*256 + t) + i%8
-//   VEC fp32 : 4 * (chunk*2048 + (i/4)*256 + t) + i%4
-//   scalar   : chunk*8192 + i*256 + t
-// so every wavefront load is contiguous (16 B per lane, or 2/4 B per lane in
-// the scalar layout) and a thread's valid elements are a prefix of z.
-template <int DT, bool VEC>
-struct Layout;
-
-template <>
-struct Layout<DSDE_BF16, true> {
-  static constexpr int kVecElts = 8;
-  __device__ static int64_t index(int64_t chunk, int i, int t) {
-    return 8 * (chunk * 1024 + (i / 8) * 256 + t) + (i % 8);
-  }
-};
-template <>
-struct Layout<DSDE_FP32, true> {
-  static constexpr int kVecElts = 4;
-  __device__ static int64_t index(int64_t chunk, int i, int t) {
-    return 4 * (chunk * 2048 + (i / 4) * 256 + t) + (i % 4);
-  }
-};
-template <int DT>
-struct Layout<DT, false> {
-  static constexpr int kVecElts = 1;
-  __device__ static int64_t index(int64_t chunk, int i, int t) { return chunk * kChunk + int64_t(i) * 256 + t; }
-};
-
-template <int DT, bool VEC>
-__device__ __forceinline__ int load_chunk(const void *row, int64_t V, int64_t chunk, int t, float (&z)[kEltsPerThread]) {
-  int n = 0;
-  if constexpr (VEC && DT == DSDE_BF16) {
-    const uint4 *p = (const uint4 *)row;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int64_t vi = chunk * 1024 + g * 256 + t;
-      if (vi * 8 < V) {
-        const uint4 w = p[vi];
-        z[g * 8 + 0] = bf_lo(w.x);
-        z[g * 8 + 1] = bf_hi(w.x);
-        z[g * 8 + 2] = bf_lo(w.y);
-        z[g * 8 + 3] = bf_hi(w.y);
-        z[g * 8 + 4] = bf_lo(w.z);
-        z[g * 8 + 5] = bf_hi(w.z);
-        z[g * 8 + 6] = bf_lo(w.w);
-        z[g * 8 + 7] = bf_hi(w.w);
-        n += 8;
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) z[g * 8 + e] = -INFINITY;
-      }
-    }
-  } else if constexpr (VEC) {
-    const float4 *p = (const float4 *)row;
-#pragma unroll
-    for (int g = 0; g < 8; ++g) {
-      const int64_t vi = chunk * 2048 + g * 256 + t;
-      if (vi * 4 < V) {
-        const float4 w = p[vi];
-        z[g * 4 + 0] = w.x;
-        z[g * 4 + 1] = w.y;
-        z[g * 4 + 2] = w.z;
-        z[g * 4 + 3] = w.w;
-        n += 4;
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) z[g * 4 + e] = -INFINITY;
-      }
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < kEltsPerThread; ++i) {
-      const int64_t v = chunk * kChunk + int64_t(i) * 256 + t;
-      if (v < V) {
-        z[i] = load_logit(row, DT, v);
-        ++n;
-      } else {
-        z[i] = -INFINITY;
-      }
-    }
-  }
-  return n;
-}
-
 // Block-wide max of one value per thread (all threads receive it).
 __device__ __forceinline__ float block_max(float v, float *lds) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -152,47 +77,166 @@ __device__ __forceinline__ float block_max(float v, float *lds) {
 }
 
 // ---------------------------------------------------------------------------
+// chunk of a row held by one workgroup
+// ---------------------------------------------------------------------------
+//
+// The 8192 logits of chunk k of a row are spread over the 256 threads so that
+// each wavefront load is contiguous.  Thread t owns slots i = 0..31:
+//   bf16, 16-byte rows : logit 8 * (1024 k + 256 (i / 8) + t) + i % 8  (4 x uint4)
+//   fp32, 16-byte rows : logit 4 * (2048 k + 256 (i / 4) + t) + i % 4  (8 x float4)
+//   any other row      : logit 8192 k + 256 i + t                       (32 scalars)
+// Every load uses an in-bounds (clamped) index and the value is replaced by
+// padding past V, so the loads never branch.
+
+template <int DT, bool VEC>
+struct Layout;
+template <>
+struct Layout<DSDE_BF16, true> {
+  static constexpr int kVec = 8;
+  __device__ static int64_t index(int64_t chunk, int i, int t) {
+    return 8 * (chunk * 1024 + (i / 8) * 256 + t) + (i % 8);
+  }
+  __device__ static void owner(int64_t local, int *t, int *i) {
+    *t = int((local >> 3) & 255);
+    *i = int((local >> 11) * 8 + (local & 7));
+  }
+};
+template <>
+struct Layout<DSDE_FP32, true> {
+  static constexpr int kVec = 4;
+  __device__ static int64_t index(int64_t chunk, int i, int t) {
+    return 4 * (chunk * 2048 + (i / 4) * 256 + t) + (i % 4);
+  }
+  __device__ static void owner(int64_t local, int *t, int *i) {
+    *t = int((local >> 2) & 255);
+    *i = int((local >> 10) * 4 + (local & 3));
+  }
+};
+template <int DT>
+struct Layout<DT, false> {
+  static constexpr int kVec = 1;
+  __device__ static int64_t index(int64_t chunk, int i, int t) { return chunk * kChunk + int64_t(i) * 256 + t; }
+  __device__ static void owner(int64_t local, int *t, int *i) {
+    *t = int(local & 255);
+    *i = int(local >> 8);
+  }
+};
+
+// Raw bf16 chunk of one row: 4 x uint4 per thread.
+struct RawBf16 {
+  uint4 v0, v1, v2, v3;
+};
+
+__device__ __forceinline__ RawBf16 load_raw_bf16(const void *row, int64_t V, int64_t chunk, int t) {
+  const uint4 *p = (const uint4 *)row;
+  const int64_t last = V / 8 - 1;
+  const int64_t i0 = chunk * 1024 + t;
+  const uint4 pad = make_uint4(kPadBf16x2, kPadBf16x2, kPadBf16x2, kPadBf16x2);
+  const uint4 a0 = p[min(i0, last)], a1 = p[min(i0 + 256, last)];
+  const uint4 a2 = p[min(i0 + 512, last)], a3 = p[min(i0 + 768, last)];
+  RawBf16 r;
+  r.v0 = i0 <= last ? a0 : pad;
+  r.v1 = i0 + 256 <= last ? a1 : pad;
+  r.v2 = i0 + 512 <= last ? a2 : pad;
+  r.v3 = i0 + 768 <= last ? a3 : pad;
+  return r;
+}
+
+__device__ __forceinline__ float max2(uint32_t w) { return fmaxf(bf_lo(w), bf_hi(w)); }
+__device__ __forceinline__ float vmax(uint4 v) {
+  return fmaxf(fmaxf(max2(v.x), max2(v.y)), fmaxf(max2(v.z), max2(v.w)));
+}
+__device__ __forceinline__ float raw_max(const RawBf16 &r) {
+  return fmaxf(fmaxf(vmax(r.v0), vmax(r.v1)), fmaxf(vmax(r.v2), vmax(r.v3)));
+}
+__device__ __forceinline__ float pick_bf16(const RawBf16 &r, int i) {
+  const uint4 v = (i >> 3) == 0 ? r.v0 : (i >> 3) == 1 ? r.v1 : (i >> 3) == 2 ? r.v2 : r.v3;
+  const int w = (i >> 1) & 3;
+  const uint32_t x = w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
+  return (i & 1) ? bf_hi(x) : bf_lo(x);
+}
+
+// Statistics of one logit pair with references rt, rd (log2 domain).
+__device__ __forceinline__ void acc_pair(float zt, float zd, float c, float rt, float rd, float &sp, float &sq,
+                                         float &a) {
+  const float at = fmaf(zt, c, -rt), ad = fmaf(zd, c, -rd);
+  const float et = fast_exp2(at), ed = fast_exp2(ad);
+  sp += et;
+  sq += ed;
+  a = fmaf(et, at - ad, a);
+}
+__device__ __forceinline__ void acc_word(uint32_t t, uint32_t d, float c, float rt, float rd, float (&s)[6]) {
+  acc_pair(bf_lo(t), bf_lo(d), c, rt, rd, s[0], s[1], s[2]);
+  acc_pair(bf_hi(t), bf_hi(d), c, rt, rd, s[3], s[4], s[5]);
+}
+__device__ __forceinline__ void acc_vec(uint4 t, uint4 d, float c, float rt, float rd, float (&s)[6]) {
+  acc_word(t.x, d.x, c, rt, rd, s);
+  acc_word(t.y, d.y, c, rt, rd, s);
+  acc_word(t.z, d.z, c, rt, rd, s);
+  acc_word(t.w, d.w, c, rt, rd, s);
+}
+
+// Generic chunk of one row as 32 floats (fp32 rows, or rows without 16-byte alignment).
+template <int DT, bool VEC>
+__device__ __forceinline__ void load_chunk_f32(const void *row, int64_t V, int64_t chunk, int t,
+                                               float (&z)[kEltsPerThread]) {
+  if constexpr (VEC && DT == DSDE_FP32) {
+    const float4 *p = (const float4 *)row;
+    const int64_t last = V / 4 - 1;
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      const int64_t i = chunk * 2048 + g * 256 + t;
+      const float4 w = p[min(i, last)];
+      const bool ok = i <= last;
+      z[g * 4 + 0] = ok ? w.x : kPadF32;
+      z[g * 4 + 1] = ok ? w.y : kPadF32;
+      z[g * 4 + 2] = ok ? w.z : kPadF32;
+      z[g * 4 + 3] = ok ? w.w : kPadF32;
+    }
+  } else if constexpr (VEC && DT == DSDE_BF16) {
+    const RawBf16 r = load_raw_bf16(row, V, chunk, t);
+#pragma unroll
+    for (int i = 0; i < kEltsPerThread; ++i) z[i] = pick_bf16(r, i);
+  } else {
+#pragma unroll
+    for (int i = 0; i < kEltsPerThread; ++i) {
+      const int64_t v = chunk * kChunk + int64_t(i) * 256 + t;
+      const float x = load_logit(row, DT, v < V ? v : V - 1);
+      z[i] = v < V ? x : kPadF32;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // set-up
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(1024) void setup_kernel(int64_t V, int32_t B, int64_t N, int32_t k_max,
+__global__ __launch_bounds__(1024) void setup_kernel(int32_t B, int64_t N, int32_t k_max,
                                                      const int32_t *__restrict__ sl,
                                                      const int32_t *__restrict__ cu_sl,
-                                                     const int32_t *__restrict__ draft_tokens,
                                                      const float *__restrict__ temperature,
-                                                     const float *__restrict__ u_acc,
-                                                     const float *__restrict__ u_res, uint32_t *__restrict__ seq_err,
-                                                     PairInfo *__restrict__ pinfo) {
+                                                     uint32_t *__restrict__ seq_err, WorkItem *__restrict__ work) {
+  const int t = threadIdx.x;
+  const int64_t c_first = cu_sl[0], c_last = cu_sl[B];
   int bad = 0;
-  for (int32_t b = threadIdx.x; b < B; b += blockDim.x) {
+  for (int32_t b = t; b < B; b += blockDim.x) {
     const int64_t s = sl[b];
     if (s < 0 || s > k_max || int64_t(cu_sl[b + 1]) - int64_t(cu_sl[b]) != s) bad = 1;
   }
   bad = __syncthreads_or(bad);
-  if (cu_sl[0] != 0 || int64_t(cu_sl[B]) != N) bad = 1;
-
+  if (c_first != 0 || c_last != N) bad = 1;
   if (bad) {
-    for (int32_t b = threadIdx.x; b < B; b += blockDim.x) seq_err[b] = DSDE_ERR_LAYOUT;
-    for (int64_t i = threadIdx.x; i < N; i += blockDim.x) pinfo[i] = PairInfo{-1, 0};
+    for (int32_t b = t; b < B; b += blockDim.x) seq_err[b] = DSDE_ERR_LAYOUT;
+    for (int64_t k = t; k < N; k += blockDim.x) work[k] = WorkItem{int32_t(k), -1, 0u, 0};
     return;
   }
-  for (int32_t b = threadIdx.x; b < B; b += blockDim.x) {
+  for (int32_t b = t; b < B; b += blockDim.x) {
     const int32_t first = cu_sl[b], s = sl[b];
-    uint32_t e = 0;
-    const float T = temperature[b];
-    if (!(isfinite(T) && T > 0.0f)) e |= DSDE_ERR_TEMP;
-    const float ur = u_res[b];
-    if (!(ur >= 0.0f && ur < 1.0f)) e |= DSDE_ERR_UNIFORM;
-    for (int32_t j = 0; j < s; ++j) {
-      const int32_t x = draft_tokens[first + j];
-      if (x < 0 || int64_t(x) >= V) e |= DSDE_ERR_TOKEN;
-      const float u = u_acc[first + j];
-      if (!(u >= 0.0f && u < 1.0f)) e |= DSDE_ERR_UNIFORM;
-    }
-    seq_err[b] = e;
-    const float c = e ? 0.0f : kLog2e / T;
-    for (int32_t j = 0; j < s; ++j)
-      pinfo[first + j] = PairInfo{e ? -1 : first + b + j, int32_t(__float_as_uint(c))};
+    seq_err[b] = 0u;
+    // the same expression as every later kernel's scale; a temperature outside
+    // the admissible range is flagged by the acceptance kernel
+    const uint32_t cbits = __float_as_uint(kLog2e / temperature[b]);
+    for (int32_t j = 0; j < s; ++j) work[first + j] = WorkItem{first + j, first + b + j, cbits, 0};
   }
 }
 
@@ -200,67 +244,13 @@ __global__ __launch_bounds__(1024) void setup_kernel(int64_t V, int32_t B, int64
 // row statistics of every drafted pair
 // ---------------------------------------------------------------------------
 
-template <int DT, bool VEC>
-__global__ __launch_bounds__(kThreads) void pair_stats_kernel(const void *__restrict__ target,
-                                                              const void *__restrict__ draft, int64_t V, int32_t nc,
-                                                              const PairInfo *__restrict__ pinfo,
-                                                              PairChunk *__restrict__ out) {
-  __shared__ float red[5][kWaves];
-  const int64_t unit = blockIdx.x;
-  const int64_t pair = unit / nc;
-  const int64_t chunk = unit - pair * nc;
-  const PairInfo pi = pinfo[pair];
-  if (pi.target_row < 0) return;
-  const float c = __uint_as_float(uint32_t(pi.scale_bits));
-  const size_t esz = DT == DSDE_BF16 ? 2 : 4;
-  const int t = threadIdx.x;
-  const char *trow = (const char *)target + size_t(pi.target_row) * size_t(V) * esz;
-  const char *drow = (const char *)draft + size_t(pair) * size_t(V) * esz;
-
-  float zt[kEltsPerThread], zd[kEltsPerThread];
-  const int n = load_chunk<DT, VEC>(trow, V, chunk, t, zt);
-  load_chunk<DT, VEC>(drow, V, chunk, t, zd);
-
-  // chunk maxima -> reference shifts used by every exponential of the chunk
-  float mt = -INFINITY, md = -INFINITY;
-#pragma unroll
-  for (int i = 0; i < kEltsPerThread; ++i) {
-    mt = fmaxf(mt, zt[i]);
-    md = fmaxf(md, zd[i]);
-  }
-  const float Mt = block_max(mt, red[0]);
-  const float Md = block_max(md, red[1]);
-  const float rt = Mt * c, rd = Md * c;
-
-  float sp0 = 0.f, sp1 = 0.f, sq0 = 0.f, sq1 = 0.f, a0 = 0.f, a1 = 0.f;
-  if (n == kEltsPerThread) {
-#pragma unroll
-    for (int i = 0; i < kEltsPerThread; i += 2) {
-      const float at0 = fmaf(zt[i], c, -rt), ad0 = fmaf(zd[i], c, -rd);
-      const float at1 = fmaf(zt[i + 1], c, -rt), ad1 = fmaf(zd[i + 1], c, -rd);
-      const float et0 = fast_exp2(at0), ed0 = fast_exp2(ad0);
-      const float et1 = fast_exp2(at1), ed1 = fast_exp2(ad1);
-      sp0 += et0;
-      sq0 += ed0;
-      a0 = fmaf(et0, at0 - ad0, a0);
-      sp1 += et1;
-      sq1 += ed1;
-      a1 = fmaf(et1, at1 - ad1, a1);
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < kEltsPerThread; ++i) {
-      if (i < n) {  // the padding must not reach the KL accumulator (0 * NaN)
-        const float at = fmaf(zt[i], c, -rt), ad = fmaf(zd[i], c, -rd);
-        const float et = fast_exp2(at), ed = fast_exp2(ad);
-        sp0 += et;
-        sq0 += ed;
-        a0 = fmaf(et, at - ad, a0);
-      }
-    }
-  }
-  const float sp = wave_sum(sp0 + sp1), sq = wave_sum(sq0 + sq1), a = wave_sum(a0 + a1);
-  const int wave = t >> 6, lane = t & 63;
+// Chunk sums of one workgroup -> one PairChunk (fixed order: lanes, then waves in fp64).
+__device__ __forceinline__ void write_pair_chunk(float rt, float rd, float sp, float sq, float a, float (*red)[kWaves],
+                                                 PairChunk *out) {
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  sp = wave_sum(sp);
+  sq = wave_sum(sq);
+  a = wave_sum(a);
   if (lane == 0) {
     red[2][wave] = sp;
     red[3][wave] = sq;
@@ -268,181 +258,374 @@ __global__ __launch_bounds__(kThreads) void pair_stats_kernel(const void *__rest
   }
   __syncthreads();
   if (t == 0) {
-    double s_p = 0.0, s_q = 0.0, s_a = 0.0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      s_p += double(red[2][w]);
-      s_q += double(red[3][w]);
-      s_a += double(red[4][w]);
-    }
     PairChunk pc;
     pc.mt = rt;
     pc.md = rd;
-    pc.pad0 = pc.pad1 = 0.f;
-    pc.sp = s_p;
-    pc.sq = s_q;
-    pc.a = s_a;
-    pc.pad2 = 0.0;
-    out[unit] = pc;
+    pc.sp = pc.sq = pc.a = 0.0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      pc.sp += double(red[2][w]);
+      pc.sq += double(red[3][w]);
+      pc.a += double(red[4][w]);
+    }
+    *out = pc;
   }
 }
 
+// bf16 rows with 16-byte alignment: the hot kernel.
+__global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__restrict__ target,
+                                                             const void *__restrict__ draft, int64_t V, int32_t nc,
+                                                             const WorkItem *__restrict__ work,
+                                                             const int32_t *__restrict__ draft_tokens,
+                                                             PairChunk *__restrict__ out,
+                                                             Gathered *__restrict__ gathered) {
+  __shared__ float red[5][kWaves];
+  const int64_t unit = blockIdx.x;
+  const int64_t k = unit / nc;
+  const int64_t chunk = unit - k * nc;
+  const WorkItem w = work[k];
+  if (w.target_row < 0) return;
+  const int t = threadIdx.x;
+  const float c = __uint_as_float(w.scale_bits);
+  const char *trow = (const char *)target + size_t(w.target_row) * size_t(V) * 2;
+  const char *drow = (const char *)draft + size_t(w.pair) * size_t(V) * 2;
+  const RawBf16 rt_ = load_raw_bf16(trow, V, chunk, t);
+  const RawBf16 rd_ = load_raw_bf16(drow, V, chunk, t);
+
+  // chunk maxima -> the reference shifts every exponential of the chunk uses
+  const float Mt = block_max(raw_max(rt_), red[0]);
+  const float Md = block_max(raw_max(rd_), red[1]);
+  const float rt = Mt * c, rd = Md * c;
+  float s[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  acc_vec(rt_.v0, rd_.v0, c, rt, rd, s);
+  acc_vec(rt_.v1, rd_.v1, c, rt, rd, s);
+  acc_vec(rt_.v2, rd_.v2, c, rt, rd, s);
+  acc_vec(rt_.v3, rd_.v3, c, rt, rd, s);
+
+  // the logits at the drafted token, from registers
+  // a token outside [0, V) never matches (its sequence is flagged later)
+  const int64_t local = int64_t(draft_tokens[w.pair]) - chunk * kChunk;
+  if (local >= 0 && local < kChunk) {
+    int ot, oi;
+    Layout<DSDE_BF16, true>::owner(local, &ot, &oi);
+    if (t == ot) {
+      // select with compile-time slots only: a runtime index into the
+      // register arrays would put them in scratch memory
+      float a = 0.f, b = 0.f;
+#pragma unroll
+      for (int i = 0; i < kEltsPerThread; ++i)
+        if (i == oi) {
+          a = pick_bf16(rt_, i);
+          b = pick_bf16(rd_, i);
+        }
+      gathered[w.pair] = Gathered{a, b};
+    }
+  }
+  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.pair) * nc + chunk);
+}
+
+// fp32 rows, or rows without 16-byte alignment.
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__restrict__ target,
+                                                                const void *__restrict__ draft, int64_t V,
+                                                                int32_t nc, const WorkItem *__restrict__ work,
+                                                                const int32_t *__restrict__ draft_tokens,
+                                                                PairChunk *__restrict__ out,
+                                                                Gathered *__restrict__ gathered) {
+  __shared__ float red[5][kWaves];
+  const int64_t unit = blockIdx.x;
+  const int64_t k = unit / nc;
+  const int64_t chunk = unit - k * nc;
+  const WorkItem w = work[k];
+  if (w.target_row < 0) return;
+  const int t = threadIdx.x;
+  const float c = __uint_as_float(w.scale_bits);
+  const size_t esz = DT == DSDE_BF16 ? 2 : 4;
+  const char *trow = (const char *)target + size_t(w.target_row) * size_t(V) * esz;
+  const char *drow = (const char *)draft + size_t(w.pair) * size_t(V) * esz;
+  float zt[kEltsPerThread], zd[kEltsPerThread];
+  load_chunk_f32<DT, VEC>(trow, V, chunk, t, zt);
+  load_chunk_f32<DT, VEC>(drow, V, chunk, t, zd);
+  float mt = zt[0], md = zd[0];
+#pragma unroll
+  for (int i = 1; i < kEltsPerThread; ++i) {
+    mt = fmaxf(mt, zt[i]);
+    md = fmaxf(md, zd[i]);
+  }
+  const float Mt = block_max(mt, red[0]);
+  const float Md = block_max(md, red[1]);
+  const float rt = Mt * c, rd = Md * c;
+  float s[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < kEltsPerThread; i += 2) {
+    acc_pair(zt[i], zd[i], c, rt, rd, s[0], s[1], s[2]);
+    acc_pair(zt[i + 1], zd[i + 1], c, rt, rd, s[3], s[4], s[5]);
+  }
+  // a token outside [0, V) never matches (its sequence is flagged later)
+  const int64_t local = int64_t(draft_tokens[w.pair]) - chunk * kChunk;
+  if (local >= 0 && local < kChunk) {
+    int ot, oi;
+    Layout<DT, VEC>::owner(local, &ot, &oi);
+    if (t == ot) {
+      float a = 0.f, b = 0.f;
+#pragma unroll
+      for (int i = 0; i < kEltsPerThread; ++i)
+        if (i == oi) {
+          a = zt[i];
+          b = zd[i];
+        }
+      gathered[w.pair] = Gathered{a, b};
+    }
+  }
+  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.pair) * nc + chunk);
+}
+
 // ---------------------------------------------------------------------------
-// acceptance scan
+// acceptance (+ fused signal update)
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(256) void accept_kernel(const void *__restrict__ target, const void *__restrict__ draft,
-                                                     int32_t dtype, int64_t V, int32_t B, int32_t k_max, int32_t nc,
-                                                     const int32_t *__restrict__ sl, const int32_t *__restrict__ cu_sl,
-                                                     const int32_t *__restrict__ draft_tokens,
-                                                     const float *__restrict__ temperature,
-                                                     const float *__restrict__ u_acc, const float *__restrict__ u_res,
-                                                     int32_t pad_id, const PairInfo *__restrict__ pinfo,
-                                                     const PairChunk *__restrict__ part, int32_t *__restrict__ accepted,
-                                                     int32_t *__restrict__ tokens, float *__restrict__ kld,
-                                                     uint32_t *__restrict__ seq_err, double *__restrict__ row_lse,
-                                                     DrawJob *__restrict__ jobs) {
-  const int lane = threadIdx.x & 63;
-  const int32_t b = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (b >= B) return;
-  const int32_t width = k_max + 1;
-  int32_t *tok = tokens + int64_t(b) * width;
-  uint32_t err = seq_err[b];
+struct StepParams {
+  const void *target, *draft;
+  int64_t V;
+  int32_t B, k_max, nc, pad_id;
+  const int32_t *sl, *cu_sl, *draft_tokens;
+  const float *temperature, *u_acc, *u_res;
+  int32_t *accepted, *tokens;
+  float *kld;
+  uint32_t *seq_err;
+  double *row_lse;
+  const PairChunk *part;
+  const Gathered *gathered;
+  DrawJob *jobs;
+  DrawChunk *dchunks;
+};
+
+// xor-butterfly reductions inside aligned groups of G lanes (G a power of two)
+template <int G>
+__device__ __forceinline__ float group_max(float v) {
+#pragma unroll
+  for (int o = G / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+template <int G>
+__device__ __forceinline__ double group_sum(double v) {
+#pragma unroll
+  for (int o = G / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Combines the chunk partials of every drafted pair of one sequence: groups of
+// G lanes, one pair per group, lane g of a group folds chunks g, g + G, ...
+// Results go to LDS (st_*[j] for position j).
+template <int G>
+__device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t first, int32_t s, int32_t nc,
+                                     float *st_mt, float *st_md, double *st_sp, double *st_sq, double *st_a,
+                                     int *st_bad) {
+  constexpr int P = 64 / G;  // pairs per wavefront
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane % G;
+  for (int32_t base = 0; base < s; base += kWaves * P) {
+    const int32_t j = base + wave * P + lane / G;
+    float lmt = -INFINITY, lmd = -INFINITY;
+    double lsp = 0.0, lsq = 0.0, la = 0.0;
+    if (j < s) {
+      for (int32_t ch = g; ch < nc; ch += G) {
+        const PairChunk q = part[(first + j) * nc + ch];
+        if (lmt == -INFINITY) {
+          lmt = q.mt;
+          lmd = q.md;
+          lsp = q.sp;
+          lsq = q.sq;
+          la = q.a;
+        } else {
+          const float nt = fmaxf(lmt, q.mt), nd = fmaxf(lmd, q.md);
+          const double d0t = double(lmt) - nt, d0d = double(lmd) - nd;
+          const double d1t = double(q.mt) - nt, d1d = double(q.md) - nd;
+          const double f0t = exp2(d0t), f0d = exp2(d0d), f1t = exp2(d1t), f1d = exp2(d1d);
+          la = f0t * (la + lsp * (d0t - d0d)) + f1t * (q.a + q.sp * (d1t - d1d));
+          lsp = f0t * lsp + f1t * q.sp;
+          lsq = f0d * lsq + f1d * q.sq;
+          lmt = nt;
+          lmd = nd;
+        }
+      }
+    }
+    const float mt = group_max<G>(lmt), md = group_max<G>(lmd);
+    double tsp = 0.0, tsq = 0.0, ta = 0.0;
+    if (lmt != -INFINITY) {
+      const double dt = double(lmt) - double(mt), dd = double(lmd) - double(md);
+      const double ft = exp2(dt), fd = exp2(dd);
+      tsp = lsp * ft;
+      tsq = lsq * fd;
+      ta = ft * (la + lsp * (dt - dd));
+    }
+    tsp = group_sum<G>(tsp);
+    tsq = group_sum<G>(tsq);
+    ta = group_sum<G>(ta);
+    if (j < s && g == 0) {
+      st_mt[j] = mt;
+      st_md[j] = md;
+      st_sp[j] = tsp;
+      st_sq[j] = tsq;
+      st_a[j] = ta;
+      st_bad[j] = !(isfinite(mt) && isfinite(md) && isfinite(tsp) && isfinite(tsq) && isfinite(ta));
+    }
+  }
+}
+
+template <bool FUSED>
+__global__ __launch_bounds__(kThreads) void accept_kernel(const StepParams P, const SignalArgs S) {
+  __shared__ float st_mt[DSDE_MAX_K + 1], st_md[DSDE_MAX_K + 1];
+  __shared__ double st_sp[DSDE_MAX_K + 1], st_sq[DSDE_MAX_K + 1], st_a[DSDE_MAX_K + 1];
+  __shared__ int st_bad[DSDE_MAX_K + 1];
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int32_t b = blockIdx.x;
+  const int32_t width = P.k_max + 1;
+  int32_t *tok = P.tokens + int64_t(b) * width;
   DrawJob none{};
   none.kind = -1;
+  uint32_t err = P.seq_err[b];
   if (err & DSDE_ERR_LAYOUT) {
-    if (lane < width) tok[lane] = pad_id;
-    if (lane == 0) {
-      accepted[b] = 0;
-      jobs[b] = none;
+    if (t < width) tok[t] = P.pad_id;
+    if (t == 0) {
+      P.accepted[b] = 0;
+      P.jobs[b] = none;
+      if constexpr (FUSED) S.mu_last[b] = S.var_short[b] = S.var_long[b] = S.wvir[b] = S.sf[b] = NAN;
     }
     return;
   }
-  const int32_t s = sl[b], first = cu_sl[b];
-  const bool active = lane < s;
-  const int64_t i = first + lane;
-
-  float mt = -INFINITY, md = -INFINITY;
-  double sp = 0.0, sq = 0.0, acc_a = 0.0;
-  bool bad = false;
-  if (active && !err) {
-    const PairChunk *pc = part + i * nc;
-    for (int32_t ch = 0; ch < nc; ++ch) {
-      mt = fmaxf(mt, pc[ch].mt);
-      md = fmaxf(md, pc[ch].md);
-    }
-    for (int32_t ch = 0; ch < nc; ++ch) {
-      const PairChunk q = pc[ch];
-      const double dt = double(q.mt) - double(mt), dd = double(q.md) - double(md);
-      const double ft = exp2(dt), fd = exp2(dd);
-      sp += q.sp * ft;
-      sq += q.sq * fd;
-      acc_a += ft * (q.a + q.sp * (dt - dd));
-    }
-    bad = !(isfinite(mt) && isfinite(md) && isfinite(sp) && isfinite(sq) && isfinite(acc_a));
-  }
-  if (__ballot(bad)) err |= DSDE_ERR_LOGIT;
-
-  if (err) {
-    if (lane < width) tok[lane] = pad_id;
-    if (active) kld[i] = NAN;
-    if (lane == 0) {
-      accepted[b] = 0;
-      seq_err[b] = err;
-      jobs[b] = none;
-    }
-    return;
-  }
-
-  const float c = active ? __uint_as_float(uint32_t(pinfo[i].scale_bits)) : 0.f;
-  bool ok = false;
+  const int32_t s = P.sl[b], first = P.cu_sl[b];
+  const float T = P.temperature[b], ur = P.u_res[b];
+  // per-position inputs of wave 0 (lane j = drafted position j), fetched
+  // together with the chunk partials below
   int32_t x = 0;
+  float u = 0.f;
+  Gathered gz{0.f, 0.f};
+  if (wave == 0 && lane < s) {
+    x = P.draft_tokens[first + lane];
+    u = P.u_acc[first + lane];
+    gz = P.gathered[first + lane];
+  }
+  // row statistics of every drafted pair (read even for a flagged sequence:
+  // the layout is valid, so every access stays in bounds)
+  if (s > 0) {
+    if (P.nc <= 16)
+      combine_pairs<16>(P.part, first, s, P.nc, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
+    else if (P.nc <= 32)
+      combine_pairs<32>(P.part, first, s, P.nc, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
+    else
+      combine_pairs<64>(P.part, first, s, P.nc, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  // per-sequence input checks
+  {
+    uint32_t e = 0;
+    if (lane < s) {
+      if (x < 0 || int64_t(x) >= P.V) e |= DSDE_ERR_TOKEN;
+      if (!(u >= 0.0f && u < 1.0f)) e |= DSDE_ERR_UNIFORM;
+    }
+    for (int32_t j = lane + 64; j < s; j += 64) {  // only when k_max > 63 would allow it
+      const int32_t xj = P.draft_tokens[first + j];
+      if (xj < 0 || int64_t(xj) >= P.V) e |= DSDE_ERR_TOKEN;
+    }
+    if (lane == 0) {
+      if (!(T >= kMinTemp && T <= kMaxTemp)) e |= DSDE_ERR_TEMP;
+      if (!(ur >= 0.0f && ur < 1.0f)) e |= DSDE_ERR_UNIFORM;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) e |= __shfl_xor(e, o);
+    err |= e;
+  }
+  const float c = kLog2e / T;  // the same expression as the set-up's scale
+  const bool active = lane < s && !err;
+  bool ok = false, bad = false;
+  float my_kld = 0.f;
   if (active) {
+    bad = st_bad[lane] != 0;
+    const double sp = st_sp[lane], sq = st_sq[lane];
     const double l2sp = log2(sp), l2sq = log2(sq);
     // KL in log2 units: E_p[(z_t c - mt) - (z_d c - md)] - log2 S_p + log2 S_q
-    const double kl2 = acc_a / sp - l2sp + l2sq;
-    const double kl = kl2 * kLn2;
-    kld[i] = kl > 0.0 ? float(kl) : 0.0f;
-    if (row_lse) {
-      row_lse[2 * i] = (double(mt) + l2sp) * kLn2;
-      row_lse[2 * i + 1] = (double(md) + l2sq) * kLn2;
+    const double kl = (st_a[lane] / sp - l2sp + l2sq) * kLn2;
+    my_kld = kl > 0.0 ? float(kl) : 0.0f;
+    // log2 p(x) - log2 q(x); z * c is exact in double
+    const double lr = (double(gz.zt) * double(c) - double(st_mt[lane]) - l2sp) -
+                      (double(gz.zd) * double(c) - double(st_md[lane]) - l2sq);
+    ok = double(u) < exp2(lr);
+    if (!bad && P.row_lse) {
+      P.row_lse[2 * (first + lane)] = (double(st_mt[lane]) + l2sp) * kLn2;
+      P.row_lse[2 * (first + lane) + 1] = (double(st_md[lane]) + l2sq) * kLn2;
     }
-    x = draft_tokens[i];
-    const int64_t trow = first + b + lane;
-    const double zt = load_logit(target, dtype, trow * V + x);
-    const double zd = load_logit(draft, dtype, i * V + x);
-    // log2 p(x) - log2 q(x), with z*c exact in double
-    const double lr = (zt * double(c) - double(mt) - l2sp) - (zd * double(c) - double(md) - l2sq);
-    ok = double(u_acc[i]) < exp2(lr);
   }
+  if (__ballot(bad)) err |= DSDE_ERR_LOGIT;
   const uint64_t mask = __ballot(ok);
   int32_t a = int32_t(__builtin_ctzll(~mask));
   if (a > s) a = s;
-  if (lane < width) tok[lane] = lane < a ? x : pad_id;
-  if (lane == 0) accepted[b] = a;
-  if (a < s) {
-    if (lane == a) {
-      DrawJob j;
-      j.kind = 0;
-      j.accepted = a;
-      j.target_row = first + b + a;
-      j.draft_row = first + a;
-      j.scale = c;
-      j.mt = mt;
-      j.md = md;
-      j.inv_sp = float(1.0 / sp);
-      j.inv_sq = float(1.0 / sq);
-      j.u = u_res[b];
-      j.pad0 = j.pad1 = 0;
-      jobs[b] = j;
-    }
-  } else if (lane == 0) {
-    DrawJob j;
-    j.kind = 1;
-    j.accepted = a;
-    j.target_row = first + b + s;
-    j.draft_row = -1;
-    j.scale = kLog2e / temperature[b];  // the same expression as the pair scale of the set-up
-    j.mt = j.md = 0.f;
-    j.inv_sp = j.inv_sq = 0.f;
-    j.u = u_res[b];
-    j.pad0 = j.pad1 = 0;
-    jobs[b] = j;
+  if (err) {
+    a = 0;
+    my_kld = NAN;
   }
+  if (lane < s) P.kld[first + lane] = my_kld;
+  if (lane < width) tok[lane] = lane < a ? x : P.pad_id;
+  if (lane == 0) {
+    P.accepted[b] = a;
+    DrawJob j = none;
+    if (!err) {
+      j.accepted = a;
+      j.scale = c;
+      j.u = ur;
+      if (a < s) {
+        j.kind = 0;
+        j.target_row = first + b + a;
+        j.draft_row = first + a;
+        j.mt = st_mt[a];
+        j.md = st_md[a];
+        j.inv_sp = float(1.0 / st_sp[a]);
+        j.inv_sq = float(1.0 / st_sq[a]);
+      } else {
+        j.kind = 1;
+        j.target_row = first + b + s;
+        j.draft_row = -1;
+      }
+    }
+    P.jobs[b] = j;
+  }
+  if constexpr (FUSED) {
+    // the signal update of Sec. 3.1.2 on the KLD values just computed
+    err |= wave_signal_update(s, first, nullptr, my_kld, S.hist + int64_t(b) * S.W, S.head + b, S.count + b, S.W,
+                              S.n_short, S.n_long, S.delta, S.eps, S.mu_last + b, S.var_short + b, S.var_long + b,
+                              S.wvir + b, S.sf + b);
+  }
+  if (lane == 0) P.seq_err[b] = err;
 }
 
 // ---------------------------------------------------------------------------
-// draw: chunk totals of the weights
+// draw chunk totals
 // ---------------------------------------------------------------------------
 
 template <int DT, bool VEC>
-__global__ __launch_bounds__(kThreads) void draw_chunk_kernel(const void *__restrict__ target,
-                                                              const void *__restrict__ draft, int64_t V, int32_t nc,
-                                                              const DrawJob *__restrict__ jobs,
-                                                              DrawChunk *__restrict__ out) {
+__global__ __launch_bounds__(kThreads) void draw_chunk_kernel(const StepParams P) {
   __shared__ float red[3][kWaves];
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const int64_t unit = blockIdx.x;
-  const int64_t b = unit / nc;
-  const int64_t chunk = unit - b * nc;
-  const DrawJob job = jobs[b];
+  const int32_t b = int32_t(unit / P.nc);
+  const int64_t chunk = unit - int64_t(b) * P.nc;
+  const DrawJob job = P.jobs[b];
   if (job.kind < 0) return;
   const size_t esz = DT == DSDE_BF16 ? 2 : 4;
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  const float c = job.scale;
-  const char *trow = (const char *)target + size_t(job.target_row) * size_t(V) * esz;
+  const char *trow = (const char *)P.target + size_t(job.target_row) * size_t(P.V) * esz;
   float zt[kEltsPerThread];
-  const int n = load_chunk<DT, VEC>(trow, V, chunk, t, zt);
-
+  load_chunk_f32<DT, VEC>(trow, P.V, chunk, t, zt);
+  DrawChunk *out = P.dchunks + unit;
   if (job.kind == 0) {
     float zd[kEltsPerThread];
-    const char *drow = (const char *)draft + size_t(job.draft_row) * size_t(V) * esz;
-    load_chunk<DT, VEC>(drow, V, chunk, t, zd);
+    const char *drow = (const char *)P.draft + size_t(job.draft_row) * size_t(P.V) * esz;
+    load_chunk_f32<DT, VEC>(drow, P.V, chunk, t, zd);
     float sw = 0.f, spp = 0.f;
 #pragma unroll
     for (int i = 0; i < kEltsPerThread; ++i) {
-      // -inf padding gives p = q = 0, hence zero weight
-      const float p = fast_exp2(fmaf(zt[i], c, -job.mt)) * job.inv_sp;
-      const float q = fast_exp2(fmaf(zd[i], c, -job.md)) * job.inv_sq;
+      // padding gives p = q = 0, hence zero weight
+      const float p = fast_exp2(fmaf(zt[i], job.scale, -job.mt)) * job.inv_sp;
+      const float q = fast_exp2(fmaf(zd[i], job.scale, -job.md)) * job.inv_sq;
       sw += fmaxf(p - q, 0.0f);
       spp += p;
     }
@@ -459,39 +642,39 @@ __global__ __launch_bounds__(kThreads) void draw_chunk_kernel(const void *__rest
         dc.w += double(red[0][w]);
         dc.p += double(red[1][w]);
       }
-      out[unit] = dc;
+      *out = dc;
     }
     return;
   }
-
-  // bonus row: chunk-local reference shift, plus detection of non-finite logits
-  float m = -INFINITY, lo = INFINITY;
+  // bonus row: chunk reference shift, and detection of non-finite logits
+  // (+inf shows in the max, NaN in the sum, -inf in the min)
+  float m = zt[0], lo = zt[0];
 #pragma unroll
-  for (int i = 0; i < kEltsPerThread; ++i) {
+  for (int i = 1; i < kEltsPerThread; ++i) {
     m = fmaxf(m, zt[i]);
-    if (i < n) lo = fminf(lo, zt[i]);
+    if (Layout<DT, VEC>::index(chunk, i, t) < P.V) lo = fminf(lo, zt[i]);
   }
-  int bad = (n > 0 && (lo == -INFINITY || m == INFINITY)) ? 1 : 0;
+  int bad = (m == INFINITY || lo == -INFINITY) ? 1 : 0;
   const float M = block_max(m, red[0]);
-  const float ref = M * c;
-  float s = 0.f;
+  const float ref = M * job.scale;
+  float sum = 0.f;
 #pragma unroll
-  for (int i = 0; i < kEltsPerThread; ++i) s += fast_exp2(fmaf(zt[i], c, -ref));
-  s = wave_sum(s);
+  for (int i = 0; i < kEltsPerThread; ++i) sum += fast_exp2(fmaf(zt[i], job.scale, -ref));
+  sum = wave_sum(sum);
   bad = __syncthreads_or(bad);
-  if (lane == 0) red[1][wave] = s;
+  if (lane == 0) red[1][wave] = sum;
   __syncthreads();
   if (t == 0) {
     DrawChunk dc{};
     for (int w = 0; w < kWaves; ++w) dc.w += double(red[1][w]);
     dc.ref = ref;
     dc.bad = bad || !isfinite(dc.w) || !isfinite(ref);
-    out[unit] = dc;
+    *out = dc;
   }
 }
 
 // ---------------------------------------------------------------------------
-// draw: locate u' * Z
+// draw: locate u' * Z (+ fused batch cap)
 // ---------------------------------------------------------------------------
 
 // Exclusive block scan of one double per thread (fixed order); returns the
@@ -516,103 +699,129 @@ __device__ double block_exclusive_scan(double v, double *lds, double *total) {
   return base + incl - v;
 }
 
-template <int DT, bool VEC>
-__global__ __launch_bounds__(kThreads) void draw_kernel(const void *__restrict__ target, const void *__restrict__ draft,
-                                                        int64_t V, int32_t nc, int32_t k_max, int32_t pad_id,
-                                                        const int32_t *__restrict__ sl,
-                                                        const int32_t *__restrict__ cu_sl,
-                                                        const DrawJob *__restrict__ jobs,
-                                                        const DrawChunk *__restrict__ chunks,
-                                                        int32_t *__restrict__ accepted, int32_t *__restrict__ tokens,
-                                                        float *__restrict__ kld, uint32_t *__restrict__ seq_err) {
+template <int DT, bool VEC, bool FUSED>
+__global__ __launch_bounds__(kThreads) void finish_kernel(const StepParams P, const SignalArgs S) {
+  constexpr int kv = Layout<DT, VEC>::kVec;
+  constexpr int kSlabs = kEltsPerThread / kv;
   __shared__ double dsh[kWaves];
+  __shared__ double s_slab[kSlabs][kWaves];
   __shared__ double s_rem;
   __shared__ int64_t s_chunk;
-  __shared__ int s_mode, s_bad, s_found;
+  __shared__ int s_mode, s_bad;
   __shared__ float s_ref;
-  __shared__ int64_t s_y, s_last;
+  __shared__ unsigned long long s_y, s_last;
   const int32_t b = blockIdx.x;
-  const DrawJob job = jobs[b];
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  if constexpr (FUSED) {
+    if (b == P.B) {
+      __shared__ double red_s[kThreads];
+      __shared__ int red_n[kThreads];
+      block_next_sl(P.B, S.sf, S.wvir, S.sl_max, S.sl_min, S.sl_hi, S.sl_hat, S.sl_cap, S.sl_next, P.seq_err,
+                    true, red_s, red_n);
+      return;
+    }
+  }
+  const DrawJob job = P.jobs[b];
   if (job.kind < 0) return;
-  const int t = threadIdx.x;
-  const DrawChunk *dc = chunks + int64_t(b) * nc;
+  const int32_t nc = P.nc;
+  const DrawChunk *dc = P.dchunks + int64_t(b) * nc;
 
-  if (t == 0) {
-    int mode = 0;  // 0: residual weights, 1: p of the rejected pair, 2: bonus exponentials
-    int bad = 0;
-    double Z = 0.0, fmax_ref = 0.0;
+  // ---- the chunk holding u' * Z: wave 0, lanes over chunks, fixed-order fp64 sums
+  if (wave == 0) {
+    int mode = job.kind == 0 ? 0 : 2;  // 0: residual weights, 1: p of the rejected pair, 2: bonus exponentials
+    // lane l folds chunks l, l + 64, ... (in order) for its part of the prefix
     float ref_max = -INFINITY;
-    if (job.kind == 0) {
-      for (int32_t ch = 0; ch < nc; ++ch) Z += dc[ch].w;
-      if (!(Z > 0.0)) {
-        mode = 1;
-        Z = 0.0;
-        for (int32_t ch = 0; ch < nc; ++ch) Z += dc[ch].p;
-      }
-    } else {
-      mode = 2;
-      for (int32_t ch = 0; ch < nc; ++ch) {
+    int bad = 0;
+    if (mode == 2) {
+      for (int32_t ch = lane; ch < nc; ch += 64) {
         bad |= dc[ch].bad;
         ref_max = fmaxf(ref_max, dc[ch].ref);
       }
-      if (!bad)
-        for (int32_t ch = 0; ch < nc; ++ch) Z += dc[ch].w * exp2(double(dc[ch].ref) - double(ref_max));
-      fmax_ref = ref_max;
+      ref_max = wave_max(ref_max);
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) bad |= __shfl_xor(bad, o);
+    }
+    auto weight = [&](int32_t ch, int m) -> double {
+      return m == 0 ? dc[ch].w : m == 1 ? dc[ch].p : dc[ch].w * exp2(double(dc[ch].ref) - double(ref_max));
+    };
+    double Z = 0.0;
+    if (!bad) {
+      double part = 0.0;
+      for (int32_t ch = lane; ch < nc; ch += 64) part += weight(ch, mode);
+      Z = wave_sum_f64(part);
+      if (mode == 0 && !(Z > 0.0)) {  // no residual mass: p of the same target row
+        mode = 1;
+        part = 0.0;
+        for (int32_t ch = lane; ch < nc; ch += 64) part += weight(ch, 1);
+        Z = wave_sum_f64(part);
+      }
     }
     const double target_mass = double(job.u) * Z;
+    // walk 64 chunks at a time: inclusive wave scan, first chunk whose cumulative exceeds the target
     int64_t found = nc - 1;
-    double before = 0.0;
+    double before = 0.0, base = 0.0;
     if (!bad) {
-      double C = 0.0;
-      for (int32_t ch = 0; ch < nc; ++ch) {
-        const double w = mode == 0 ? dc[ch].w
-                         : mode == 1 ? dc[ch].p
-                                     : dc[ch].w * exp2(double(dc[ch].ref) - fmax_ref);
-        if (C + w > target_mass) {
-          found = ch;
+      for (int32_t c0 = 0; c0 < nc; c0 += 64) {
+        const int32_t ch = c0 + lane;
+        const double w = ch < nc ? weight(ch, mode) : 0.0;
+        double incl = w;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const double y = __shfl_up(incl, o);
+          if (lane >= o) incl += y;
+        }
+        const uint64_t hit = __ballot(ch < nc && base + incl > target_mass);
+        if (hit) {
+          const int l = __builtin_ctzll(hit);
+          found = c0 + l;
+          before = base + __shfl(incl - w, l);
           break;
         }
-        C += w;
+        base += __shfl(incl, 63);
+        before = base;
       }
-      before = C;
     }
-    double rem = target_mass - before;
-    if (rem < 0.0) rem = 0.0;
-    if (mode == 2 && !bad) rem *= exp2(fmax_ref - double(dc[found].ref));  // into the chunk's own scale
-    s_rem = rem;
-    s_chunk = found;
-    s_mode = mode;
-    s_bad = bad;
-    s_ref = mode == 2 && !bad ? dc[found].ref : 0.f;
-    s_found = 0;
-    s_y = INT64_MAX;
-    s_last = 0;
+    if (lane == 0) {
+      double rem = target_mass - before;
+      if (rem < 0.0) rem = 0.0;
+      if (mode == 2 && !bad) rem *= exp2(double(ref_max) - double(dc[found].ref));  // into the chunk's own scale
+      s_rem = rem;
+      s_chunk = found;
+      s_mode = mode;
+      s_bad = bad;
+      s_ref = mode == 2 && !bad ? dc[found].ref : 0.f;
+      s_y = ~0ull;
+      s_last = 0;
+    }
   }
   __syncthreads();
-  const int32_t width = k_max + 1;
+  const int32_t width = P.k_max + 1;
   if (s_bad) {
-    if (t < width) tokens[int64_t(b) * width + t] = pad_id;
-    if (t < sl[b]) kld[cu_sl[b] + t] = NAN;
+    // a NaN or infinite logit in the bonus row: no token is emitted
+    if (t < width) P.tokens[int64_t(b) * width + t] = P.pad_id;
     if (t == 0) {
-      accepted[b] = 0;
-      seq_err[b] |= DSDE_ERR_LOGIT;
+      P.accepted[b] = 0;
+      atomicOr(&P.seq_err[b], DSDE_ERR_LOGIT);
     }
     return;
   }
 
+  // ---- the ordered scan inside that chunk
   const size_t esz = DT == DSDE_BF16 ? 2 : 4;
   const int64_t chunk = s_chunk;
   const int mode = s_mode;
   const float c = job.scale, ref = s_ref;
-  const char *trow = (const char *)target + size_t(job.target_row) * size_t(V) * esz;
-  const char *drow = job.draft_row >= 0 ? (const char *)draft + size_t(job.draft_row) * size_t(V) * esz : nullptr;
+  const char *trow = (const char *)P.target + size_t(job.target_row) * size_t(P.V) * esz;
   float zt[kEltsPerThread], zd[kEltsPerThread];
-  load_chunk<DT, VEC>(trow, V, chunk, t, zt);
-  if (mode != 2) load_chunk<DT, VEC>(drow, V, chunk, t, zd);
-
-  // weights of this thread's elements, recomputed exactly as for the chunk totals
+  load_chunk_f32<DT, VEC>(trow, P.V, chunk, t, zt);
+  if (mode != 2) {
+    const char *drow = (const char *)P.draft + size_t(job.draft_row) * size_t(P.V) * esz;
+    load_chunk_f32<DT, VEC>(drow, P.V, chunk, t, zd);
+  }
+  // weights of this thread's logits, computed exactly as for the chunk totals;
+  // slab g (ascending token order) holds slots [g*kv, (g+1)*kv) of every thread
   float w[kEltsPerThread];
-  int64_t last = -1;
+  unsigned long long last = 0;  // 1 + index of the last positive weight
 #pragma unroll
   for (int i = 0; i < kEltsPerThread; ++i) {
     float wi;
@@ -625,49 +834,70 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(const void *__restrict__
     }
     w[i] = wi;
     if (wi > 0.0f) {
-      const int64_t idx = Layout<DT, VEC>::index(chunk, i, t);
+      const unsigned long long idx = (unsigned long long)Layout<DT, VEC>::index(chunk, i, t) + 1;
       last = idx > last ? idx : last;
     }
   }
-  // slabs in ascending token order: slab g holds elements [g*kv, (g+1)*kv) of every thread
-  constexpr int kv = Layout<DT, VEC>::kVecElts;
+  double tot[kSlabs];
+#pragma unroll
+  for (int g = 0; g < kSlabs; ++g) {
+    double x = 0.0;
+#pragma unroll
+    for (int e = 0; e < kv; ++e) x += double(w[g * kv + e]);
+    tot[g] = x;
+    const double ws = wave_sum_f64(x);
+    if (lane == 0) s_slab[g][wave] = ws;
+  }
+  __syncthreads();
+  // the slab that holds the remaining mass (every thread walks the same totals)
   double rem = s_rem;
-  for (int g = 0; g < kEltsPerThread / kv; ++g) {
-    double tot = 0.0;
+  int gs = -1;
 #pragma unroll
-    for (int e = 0; e < kv; ++e) tot += double(w[g * kv + e]);
+  for (int g = 0; g < kSlabs; ++g) {
+    double st = 0.0;
+#pragma unroll
+    for (int k = 0; k < kWaves; ++k) st += s_slab[g][k];
+    if (gs < 0) {
+      if (rem < st) {
+        gs = g;
+      } else {
+        rem -= st;
+      }
+    }
+  }
+  bool found = false;
+  if (gs >= 0) {
+    double x = 0.0;
+#pragma unroll
+    for (int g = 0; g < kSlabs; ++g)
+      if (g == gs) x = tot[g];
     double slab_total;
-    const double excl = block_exclusive_scan(tot, dsh, &slab_total);
-    if (rem >= excl && rem < excl + tot) {
+    const double excl = block_exclusive_scan(x, dsh, &slab_total);
+    if (rem >= excl && rem < excl + x) {
       double acc = excl;
-      int64_t y = -1;
+      unsigned long long y = ~0ull;
 #pragma unroll
-      for (int e = 0; e < kv; ++e) {
-        acc += double(w[g * kv + e]);
-        if (y < 0 && acc > rem) y = Layout<DT, VEC>::index(chunk, g * kv + e, t);
-      }
-      if (y >= 0) {
-        atomicMin((unsigned long long *)&s_y, (unsigned long long)y);
-        s_found = 1;
-      }
+      for (int g = 0; g < kSlabs; ++g)
+        if (g == gs) {
+#pragma unroll
+          for (int e = 0; e < kv; ++e) {
+            acc += double(w[g * kv + e]);
+            if (y == ~0ull && acc > rem) y = (unsigned long long)Layout<DT, VEC>::index(chunk, g * kv + e, t);
+          }
+        }
+      if (y != ~0ull) atomicMin(&s_y, y);
     }
     __syncthreads();
-    if (s_found) break;
-    rem -= slab_total;
-    if (rem < 0.0) rem = 0.0;
+    found = s_y != ~0ull;
   }
-  if (!s_found) {
+  if (!found) {
     // rounding left u' * Z past this chunk's total: the last positive weight
-    for (int o = 32; o > 0; o >>= 1) {
-      const int64_t other = __shfl_xor(last, o);
-      last = other > last ? other : last;
-    }
-    if ((t & 63) == 0) atomicMax((unsigned long long *)&s_last, (unsigned long long)(last + 1));
+    atomicMax(&s_last, last);
     __syncthreads();
   }
   if (t == 0) {
-    const int64_t y = s_found ? s_y : (s_last > 0 ? s_last - 1 : 0);
-    tokens[int64_t(b) * width + job.accepted] = int32_t(y);
+    const unsigned long long y = found ? s_y : (s_last > 0 ? s_last - 1 : 0);
+    P.tokens[int64_t(b) * width + job.accepted] = int32_t(y);
   }
 }
 
@@ -676,51 +906,83 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(const void *__restrict__
 static inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 template <int DT, bool VEC>
-static int launch_rows(const VerifyArgs &a, const WorkspaceLayout &L, int32_t nc) {
-  char *ws = (char *)a.workspace;
-  PairInfo *pinfo = (PairInfo *)(ws + L.pair_info);
-  PairChunk *part = (PairChunk *)(ws + L.pair_chunk);
-  DrawJob *jobs = (DrawJob *)(ws + L.draw_job);
-  DrawChunk *dchunks = (DrawChunk *)(ws + L.draw_chunk);
-  hipStream_t st = a.stream;
-
-  if (a.N > 0) {
-    if (a.prof_start) (void)hipEventRecord(a.prof_start, st);
-    pair_stats_kernel<DT, VEC><<<dim3(unsigned(a.N * nc)), dim3(kThreads), 0, st>>>(a.target, a.draft, a.V, nc,
-                                                                                   pinfo, part);
-    if (a.prof_stop) (void)hipEventRecord(a.prof_stop, st);
-  }
-  accept_kernel<<<dim3(unsigned((a.B + 3) / 4)), dim3(256), 0, st>>>(
-      a.target, a.draft, a.dtype, a.V, a.B, a.k_max, nc, a.sl, a.cu_sl, a.draft_tokens, a.temperature, a.u_acc,
-      a.u_res, a.pad_id, pinfo, part, a.accepted, a.tokens, a.kld, a.seq_err, a.row_lse, jobs);
-  draw_chunk_kernel<DT, VEC><<<dim3(unsigned(int64_t(a.B) * nc)), dim3(kThreads), 0, st>>>(a.target, a.draft, a.V,
-                                                                                          nc, jobs, dchunks);
-  draw_kernel<DT, VEC><<<dim3(unsigned(a.B)), dim3(kThreads), 0, st>>>(a.target, a.draft, a.V, nc, a.k_max,
-                                                                      a.pad_id, a.sl, a.cu_sl, jobs, dchunks,
-                                                                      a.accepted, a.tokens, a.kld, a.seq_err);
-  return 0;
+static void launch_draw(const VerifyArgs &a, const StepParams &P, const SignalArgs &S, unsigned nc) {
+  draw_chunk_kernel<DT, VEC><<<dim3(unsigned(a.B) * nc), dim3(kThreads), 0, a.stream>>>(P);
+  if (a.signal)
+    finish_kernel<DT, VEC, true><<<dim3(unsigned(a.B) + 1u), dim3(kThreads), 0, a.stream>>>(P, S);
+  else
+    finish_kernel<DT, VEC, false><<<dim3(unsigned(a.B)), dim3(kThreads), 0, a.stream>>>(P, S);
 }
 
 int launch_verify(const VerifyArgs &a) {
   const WorkspaceLayout L = workspace_layout(a.B, a.N, a.V);
-  const int32_t nc = int32_t((a.V + kChunk - 1) / kChunk);
+  const int32_t nc = int32_t(num_chunks(a.V));
   char *ws = (char *)a.workspace;
-  PairInfo *pinfo = (PairInfo *)(ws + L.pair_info);
+  WorkItem *work = (WorkItem *)(ws + L.work);
+  PairChunk *part = (PairChunk *)(ws + L.pair_chunk);
+  Gathered *gath = (Gathered *)(ws + L.gathered);
   (void)hipGetLastError();
-  setup_kernel<<<dim3(1), dim3(1024), 0, a.stream>>>(a.V, a.B, a.N, a.k_max, a.sl, a.cu_sl, a.draft_tokens,
-                                                    a.temperature, a.u_acc, a.u_res, a.seq_err, pinfo);
+  setup_kernel<<<dim3(1), dim3(1024), 0, a.stream>>>(a.B, a.N, a.k_max, a.sl, a.cu_sl, a.temperature, a.seq_err,
+                                                    work);
   const bool vec = aligned16(a.target) && (a.N == 0 || aligned16(a.draft)) &&
                    (a.dtype == DSDE_BF16 ? a.V % 8 == 0 : a.V % 4 == 0);
+  if (a.N > 0) {
+    const dim3 grid(unsigned(a.N * nc));
+    if (a.prof_start) (void)hipEventRecord(a.prof_start, a.stream);
+    if (a.dtype == DSDE_BF16 && vec)
+      stats_kernel_bf16<<<grid, dim3(kThreads), 0, a.stream>>>(a.target, a.draft, a.V, nc, work, a.draft_tokens,
+                                                               part, gath);
+    else if (a.dtype == DSDE_BF16)
+      stats_kernel_generic<DSDE_BF16, false><<<grid, dim3(kThreads), 0, a.stream>>>(a.target, a.draft, a.V, nc,
+                                                                                   work, a.draft_tokens, part,
+                                                                                   gath);
+    else if (vec)
+      stats_kernel_generic<DSDE_FP32, true><<<grid, dim3(kThreads), 0, a.stream>>>(a.target, a.draft, a.V, nc,
+                                                                                  work, a.draft_tokens, part, gath);
+    else
+      stats_kernel_generic<DSDE_FP32, false><<<grid, dim3(kThreads), 0, a.stream>>>(a.target, a.draft, a.V, nc,
+                                                                                   work, a.draft_tokens, part,
+                                                                                   gath);
+    if (a.prof_stop) (void)hipEventRecord(a.prof_stop, a.stream);
+  }
+  StepParams P;
+  P.target = a.target;
+  P.draft = a.draft;
+  P.V = a.V;
+  P.B = a.B;
+  P.k_max = a.k_max;
+  P.nc = nc;
+  P.pad_id = a.pad_id;
+  P.sl = a.sl;
+  P.cu_sl = a.cu_sl;
+  P.draft_tokens = a.draft_tokens;
+  P.temperature = a.temperature;
+  P.u_acc = a.u_acc;
+  P.u_res = a.u_res;
+  P.accepted = a.accepted;
+  P.tokens = a.tokens;
+  P.kld = a.kld;
+  P.seq_err = a.seq_err;
+  P.row_lse = a.row_lse;
+  P.part = part;
+  P.gathered = gath;
+  P.jobs = (DrawJob *)(ws + L.draw_job);
+  P.dchunks = (DrawChunk *)(ws + L.draw_chunk);
+  const SignalArgs S = a.signal ? *a.signal : SignalArgs{};
+  if (a.signal)
+    accept_kernel<true><<<dim3(unsigned(a.B)), dim3(kThreads), 0, a.stream>>>(P, S);
+  else
+    accept_kernel<false><<<dim3(unsigned(a.B)), dim3(kThreads), 0, a.stream>>>(P, S);
   if (a.dtype == DSDE_BF16) {
     if (vec)
-      launch_rows<DSDE_BF16, true>(a, L, nc);
+      launch_draw<DSDE_BF16, true>(a, P, S, unsigned(nc));
     else
-      launch_rows<DSDE_BF16, false>(a, L, nc);
+      launch_draw<DSDE_BF16, false>(a, P, S, unsigned(nc));
   } else {
     if (vec)
-      launch_rows<DSDE_FP32, true>(a, L, nc);
+      launch_draw<DSDE_FP32, true>(a, P, S, unsigned(nc));
     else
-      launch_rows<DSDE_FP32, false>(a, L, nc);
+      launch_draw<DSDE_FP32, false>(a, P, S, unsigned(nc));
   }
   return hipGetLastError() == hipSuccess ? DSDE_OK : DSDE_DEVICE_ERROR;
 }

@@ -40,12 +40,21 @@ def gpu_signal(dsde, sl, cu, kld, st, n_short=10, n_long=30, delta=0.85, eps=1e-
     return {k: v.cpu().numpy() for k, v in out.items()}
 
 
-def compare_signal(got, ref, label):
+def compare_signal(got, ref, label, spread=None):
+    """Signal outputs within 1e-4 relative (variances + 1e-9 absolute), widened by the
+    oracle's first-order spread when the inputs themselves differ within the KLD
+    tolerance (chained comparisons)."""
     assert np.array_equal(got["seq_err"].astype(np.uint32), ref["seq_err"]), label
-    for k in ("mu_last", "sf", "wvir"):
-        close(got[k], ref[k], label=f"{label} {k}")
-    for k in ("var_short", "var_long"):
-        close(got[k], ref[k], abs_=1e-9, label=f"{label} {k}")
+    zero = np.zeros_like(ref["mu_last"])
+    sp = spread or {}
+    close(got["mu_last"], ref["mu_last"], abs_=0.0, label=f"{label} mu_last")
+    for k, floor in (("sf", 0.0), ("wvir", 0.0), ("var_short", 1e-9), ("var_long", 1e-9)):
+        extra = np.nan_to_num(sp.get("d_" + k, zero))
+        got_k = np.asarray(got[k], np.float64)
+        ref_k = np.asarray(ref[k], np.float64)
+        bad = ~(np.abs(got_k - ref_k) <= REL * np.abs(ref_k) + floor + extra)
+        bad &= ~(np.isnan(got_k) & np.isnan(ref_k))
+        assert not bad.any(), f"{label} {k}: {np.nonzero(bad)[0][:8]} got {got_k[bad][:4]} ref {ref_k[bad][:4]}"
 
 
 @pytest.mark.parametrize("W_, n_short, n_long", [(32, 10, 30), (8, 10, 30), (16, 3, 12), (40, 10, 30)])
@@ -120,32 +129,43 @@ def test_next_sl_alone(gpu_lib):
     print(f"[report] next_sl ties={int(ties.sum())} of {B}", flush=True)
 
 
+def oracle_chain(host, h0, hd0, c0, smax, sl_hi):
+    ref = oracle.verify(**host, n_threads=16)
+    sr = oracle.kld_signal(host["sl"], host["cu_sl"], ref["kld"], h0, hd0, c0)
+    nr = oracle.next_sl(sr["sf"], sr["wvir"], smax, 2.0, sl_hi)
+    spread = oracle.signal_spread(sr["hist"], sr["head"], sr["count"], smax, nr["seq_err"] | sr["seq_err"],
+                                  rho=1e-4)
+    return ref, sr, nr, spread
+
+
+def compare_sl(ng, nr, sr, spread, smax, sl_hi, label):
+    assert np.array_equal(ng["seq_err"].astype(np.uint32) & 32, nr["seq_err"] & 32), label
+    hat_tol = REL * np.abs(nr["sl_hat"]) + np.nan_to_num(spread["d_sl_hat"]) + 1e-6
+    ok_hat = np.isnan(nr["sl_hat"]) | (np.abs(ng["sl_hat"] - nr["sl_hat"]) <= hat_tol)
+    assert ok_hat.all(), f"{label} sl_hat: {np.nonzero(~ok_hat)[0][:8]}"
+    ties = oracle.sl_round_ties(spread["sl_hat"], spread["d_sl_hat"], nr["seq_err"], 2.0, sl_hi, tau=1e-5)
+    ok = ties == 0
+    mism = np.nonzero(ok & (ng["sl_next"] != nr["sl_next"]))[0]
+    assert mism.size == 0, f"{label}: SL decisions differ at {mism[:8]}"
+    return int(ties.sum())
+
+
 def chained_step(dsde, step, st, sl_max, sl_hi, label):
     """verify -> kld_signal -> next_sl on the GPU and the oracle's chain; compares every stage."""
     h0, hd0, c0 = st.hist.cpu().numpy(), st.head.cpu().numpy(), st.count.cpu().numpy()
     got = run_verify(dsde, step, row_lse=False)
     host = W.host_arrays(step)
-    ref = oracle.verify(**host, n_threads=16)
+    smax = sl_max.cpu().numpy().astype(np.float64)
+    ref, sr, nr, spread = oracle_chain(host, h0, hd0, c0, smax, sl_hi)
     rep = compare_verify(got, ref, host["sl"], host["cu_sl"], label)
     kld_t = torch.as_tensor(got["kld"], device="cuda")
     sg = gpu_signal(dsde, step.sl, step.cu_sl, kld_t, st)
-    sr = oracle.kld_signal(host["sl"], host["cu_sl"], ref["kld"], h0, hd0, c0)
-    # sequences the verify flagged have NaN KLD on both sides
-    compare_signal(sg, sr, f"{label} signal")
+    compare_signal(sg, sr, f"{label} signal", spread)
     dev = lambda x: torch.as_tensor(x, device="cuda")
     out = dsde.next_sl(dev(sg["sf"]), dev(sg["wvir"]), sl_max, 2.0, sl_hi)
     torch.cuda.synchronize()
     ng = {k: v.cpu().numpy() for k, v in out.items()}
-    smax = sl_max.cpu().numpy().astype(np.float64)
-    nr = oracle.next_sl(sr["sf"], sr["wvir"], smax, 2.0, sl_hi)
-    assert np.array_equal(ng["seq_err"].astype(np.uint32), nr["seq_err"])
-    close(ng["sl_hat"], nr["sl_hat"], rel=1e-3, label=f"{label} sl_hat")
-    hat, dhat = oracle.sl_hat_spread(sr["hist"], sr["head"], sr["count"], smax, nr["seq_err"], rho=1e-4)
-    ties = oracle.sl_round_ties(hat, dhat, nr["seq_err"], 2.0, sl_hi, tau=1e-5)
-    ok = ties == 0
-    mism = np.nonzero(ok & (ng["sl_next"] != nr["sl_next"]))[0]
-    assert mism.size == 0, f"{label}: SL decisions differ at {mism[:8]}"
-    rep["sl_ties"] = int(ties.sum())
+    rep["sl_ties"] = compare_sl(ng, nr, sr, spread, smax, sl_hi, label)
     return ng, nr, sr, rep
 
 
@@ -191,3 +211,52 @@ def test_controller_loop_full_shape(gpu_lib):
     cfg = W.CONFIGS["loop"]
     announce("controller loop B=1024 V=128256 3 steps")
     run_loop(gpu_lib, cfg, 3, seed=6, label="loop-full")
+
+
+def clone_state(st):
+    return W.SignalState(hist=st.hist.clone(), head=st.head.clone(), count=st.count.clone(),
+                         sl_max=st.sl_max.clone())
+
+
+@pytest.mark.parametrize("name", ["tiny", "b64", "b256"])
+def test_fused_step_equals_the_three_calls(gpu_lib, name):
+    cfg = W.CONFIGS[name]
+    step = W.make_step(cfg, seed=31, device="cuda")
+    st = W.make_signal_state(cfg, seed=31, device="cuda")
+    announce(f"fused step vs chain {name}")
+    st_a, st_b = clone_state(st), clone_state(st)
+    v = gpu_lib.verify(step.target, step.draft, step.sl, step.cu_sl, step.draft_tokens, step.temperature,
+                       step.u_acc, step.u_res, step.k_max)
+    s_ = gpu_lib.kld_signal(step.sl, step.cu_sl, v["kld"], st_a.hist, st_a.head, st_a.count)
+    n_ = gpu_lib.next_sl(s_["sf"], s_["wvir"], st_a.sl_max, 2.0, step.k_max)
+    f = gpu_lib.step(step.target, step.draft, step.sl, step.cu_sl, step.draft_tokens, step.temperature,
+                     step.u_acc, step.u_res, step.k_max, st_b.hist, st_b.head, st_b.count, st_b.sl_max)
+    torch.cuda.synchronize()
+    chain = {**v, **s_, **n_}
+    for k in ("accepted", "tokens", "sl_next"):
+        assert torch.equal(chain[k], f[k]), k
+    for k in ("kld", "mu_last", "var_short", "var_long", "wvir", "sf", "sl_hat", "sl_cap"):
+        assert torch.equal(chain[k].view(torch.int32), f[k].view(torch.int32)), k
+    assert torch.equal(st_a.hist.view(torch.int32), st_b.hist.view(torch.int32))
+    assert torch.equal(st_a.head, st_b.head) and torch.equal(st_a.count, st_b.count)
+    assert torch.equal(v["seq_err"] | s_["seq_err"] | n_["seq_err"], f["seq_err"])
+
+
+@pytest.mark.parametrize("name", ["b256", "lowacc"])
+def test_fused_step_parity(gpu_lib, name):
+    cfg = W.CONFIGS[name]
+    step = W.make_step(cfg, seed=41, device="cuda")
+    st = W.make_signal_state(cfg, seed=41, device="cuda")
+    announce(f"fused step parity {name} B={step.B} N={step.N}")
+    h0, hd0, c0 = st.hist.cpu().numpy(), st.head.cpu().numpy(), st.count.cpu().numpy()
+    f = gpu_lib.step(step.target, step.draft, step.sl, step.cu_sl, step.draft_tokens, step.temperature,
+                     step.u_acc, step.u_res, step.k_max, st.hist, st.head, st.count, st.sl_max)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in f.items()}
+    host = W.host_arrays(step)
+    smax = st.sl_max.cpu().numpy().astype(np.float64)
+    ref, sr, nr, spread = oracle_chain(host, h0, hd0, c0, smax, step.k_max)
+    rep = compare_verify(got, ref, host["sl"], host["cu_sl"], f"step {name}")
+    compare_signal({**got, "seq_err": got["seq_err"].astype(np.uint32) & 96}, sr, f"step {name} signal", spread)
+    rep["sl_ties"] = compare_sl(got, nr, sr, spread, smax, step.k_max, f"step {name}")
+    print(f"[report] fused step {name}: {rep}", flush=True)

@@ -114,7 +114,7 @@ def test_error_contract(gpu_lib):
     temps = np.ones(7, np.float32)
     tokens[2] = V                  # seq 1: token out of range
     u_acc[4] = 1.0                 # seq 2: uniform out of [0, 1)
-    temps[3] = -1.0                # seq 3: temperature
+    temps[3] = 2.0 ** 17           # seq 3: temperature outside [2^-16, 2^16]
     draft[8, 17] = np.nan          # seq 4: NaN in a drafted pair
     target[5 * 3 + 1, 40] = -np.inf  # seq 5: -inf in a drafted target row
     # seq 6: both drafts accepted (equal rows, u just below 1), bonus row has +inf
@@ -124,7 +124,8 @@ def test_error_contract(gpu_lib):
     step = step_from_arrays(target, draft, sls, tokens, temps, u_acc, u_res, 2)
     got, ref, _ = check_step(gpu_lib, step, "error contract")
     assert list(got["seq_err"]) == [0, 2, 16, 8, 4, 4, 4]
-    assert np.isnan(got["kld"][2:]).all() and np.isfinite(got["kld"][:2]).all()
+    assert np.isnan(got["kld"][2:12]).all() and np.isfinite(got["kld"][:2]).all()
+    assert np.isfinite(got["kld"][12:14]).all()  # a bad bonus row withholds only the token
 
 
 def test_bad_layout(gpu_lib):
