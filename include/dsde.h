@@ -80,6 +80,9 @@ extern "C" {
 
 /* Largest supported speculation length bound (one wavefront lane per drafted position). */
 #define DSDE_MAX_K 63
+/* Largest supported vocabulary (512 chunks of 8192 logits; the draw keeps one
+ * total per chunk on chip). */
+#define DSDE_MAX_VOCAB 4194304
 
 /* The ABI version this library implements (DSDE_ABI_VERSION). */
 int32_t dsde_abi_version(void);
@@ -100,7 +103,7 @@ size_t dsde_verify_workspace_bytes(int32_t B, int64_t N, int64_t V, int32_t k_ma
  *   draft_logits  [N, V]    dtype       draft rows (may be NULL when N = 0)
  *   dtype                               DSDE_FP32 or DSDE_BF16
  *   V, B, N, k_max                      vocabulary, sequences, drafted positions, SL bound
- *                                       (1 <= V < 2^31, B >= 1, 0 <= N <= B*k_max,
+ *                                       (1 <= V <= DSDE_MAX_VOCAB, B >= 1, 0 <= N <= B*k_max,
  *                                        0 <= k_max <= DSDE_MAX_K)
  *   sl [B], cu_sl [B+1]     int32       per-sequence SL and its exclusive prefix sums
  *   draft_tokens [N]        int32       the drafted token at each position
@@ -181,7 +184,7 @@ int32_t dsde_next_sl(int32_t B, const float *sf, const float *wvir, const float 
  * The whole step fused: dsde_verify, then dsde_kld_signal on the KLD it
  * produces, then dsde_next_sl on the signal it produces, with the arguments
  * of those three calls (see them for meaning and layout), in four kernel
- * launches instead of six.  Outputs are bit-identical to the three calls made
+ * launches instead of five.  Outputs are bit-identical to the three calls made
  * in sequence; seq_err is the OR of their error bits, except that a layout
  * error (DSDE_ERR_LAYOUT) also skips the signal update.
  * For serving loops that run the complete verification step.
@@ -196,10 +199,11 @@ int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t d
                   void *workspace, size_t workspace_bytes, void *stream);
 
 /*
- * Profiling hook: when both events are non-NULL (hipEvent_t), every later
- * dsde_verify or dsde_step records `start` just before and `stop` just after
- * its row statistics kernel (the pass that reads every drafted row pair once)
- * on its stream.  Passing NULLs turns it off.  Process-wide; not thread-safe.
+ * Profiling hook: when both events are non-NULL (hipEvent_t, created with
+ * timing enabled), every later dsde_verify or dsde_step with N > 0 launches its
+ * row statistics kernel (the pass that reads every drafted row pair once) with
+ * the two events attached to the dispatch itself, so that the elapsed time
+ * between them is that kernel's execution time.  Passing NULLs turns it off.  Process-wide; not thread-safe.
  */
 int32_t dsde_set_profile_events(void *start, void *stop);
 

@@ -231,9 +231,13 @@ def next_sl(sf, wvir, sl_max, sl_min=2.0, sl_hi=8, out=None, stream=None):
 
 
 def set_profile_events(start=None, stop=None):
-    """Record torch.cuda.Event ``start``/``stop`` around the row-statistics kernel of
-    every later ``verify`` call (None, None turns it off)."""
+    """Attach HIP events ``start``/``stop`` to the row-statistics kernel of every
+    later ``verify``/``step`` call (None, None turns it off).  Each is a
+    torch.cuda.Event or a raw hipEvent_t handle (int)."""
     lib = load()
-    s = ctypes.c_void_p(start.cuda_event) if start is not None else None
-    e = ctypes.c_void_p(stop.cuda_event) if stop is not None else None
-    _check(lib.dsde_set_profile_events(s, e))
+
+    def handle(ev):
+        if ev is None:
+            return None
+        return ctypes.c_void_p(ev if isinstance(ev, int) else ev.cuda_event)
+    _check(lib.dsde_set_profile_events(handle(start), handle(stop)))

@@ -43,39 +43,20 @@ struct Gathered {
   float zt, zd;
 };
 
-// What the draw of one sequence needs, written by the chunk-0 workgroup of
-// the draw-chunk kernel.
-struct alignas(16) DrawJob {
-  int32_t kind;        // 0: residual of the first rejected pair, 1: bonus row, -1: nothing (flagged)
-  int32_t accepted;    // a_b
-  int32_t target_row;
-  int32_t draft_row;   // -1 for the bonus row
-  float scale;         // c = log2(e) / T_b
-  float mt, md;        // row reference shifts of the rejected pair
-  float inv_sp, inv_sq;  // 1 / row sums of the rejected pair
-  float u;             // draw uniform
-  int32_t pad0, pad1;
-};
-
-// Chunk totals of the draw weights.  Residual: w = max(0, p - q) and the
-// fallback p; bonus: e = 2^(z c - ref) relative to the chunk reference.
-struct alignas(16) DrawChunk {
-  double w;
-  double p;
-  float ref;
-  int32_t bad;  // bonus: a NaN or +-inf logit was seen
-  int32_t pad0, pad1;
-};
+// Largest vocabulary: the per-sequence kernel keeps the draw-weight totals of
+// every chunk of a row in LDS.
+constexpr int kMaxChunks = 512;
+static_assert(int64_t(kMaxChunks) * kChunk == DSDE_MAX_VOCAB, "vocabulary limit of the ABI");
 
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct WorkspaceLayout {
-  size_t work, pair_chunk, gathered, draw_job, draw_chunk, total;
+  size_t work, pair_chunk, gathered, total;
 };
 
 inline int64_t num_chunks(int64_t V) { return (V + kChunk - 1) / kChunk; }
 
-inline WorkspaceLayout workspace_layout(int32_t B, int64_t N, int64_t V) {
+inline WorkspaceLayout workspace_layout(int64_t N, int64_t V) {
   const int64_t nc = num_chunks(V);
   const size_t n = size_t(N > 0 ? N : 1);
   WorkspaceLayout L;
@@ -86,10 +67,6 @@ inline WorkspaceLayout workspace_layout(int32_t B, int64_t N, int64_t V) {
   off += align_up(sizeof(PairChunk) * n * size_t(nc));
   L.gathered = off;
   off += align_up(sizeof(Gathered) * n);
-  L.draw_job = off;
-  off += align_up(sizeof(DrawJob) * size_t(B));
-  L.draw_chunk = off;
-  off += align_up(sizeof(DrawChunk) * size_t(B) * size_t(nc));
   L.total = off;
   return L;
 }
@@ -135,7 +112,7 @@ int launch_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu
                       float delta, float eps, float *mu_last, float *var_short, float *var_long, float *wvir,
                       float *sf, uint32_t *seq_err, hipStream_t stream);
 int launch_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max, float sl_min,
-                   int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
+                   int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err, bool or_err,
                    hipStream_t stream);
 
 }  // namespace dsde

@@ -6,7 +6,8 @@
 //   kld_signal_kernel  one wavefront per sequence (lanes over the window
 //                      entries); every workgroup re-checks the batch layout.
 //   next_sl_kernel     one workgroup: SL_hat per sequence, the mean cap, the
-//                      rounded and clamped next lengths.
+//                      rounded and clamped next lengths (also the last kernel
+//                      of the fused step, where it ORs its error bits).
 // Both cost their launch, not bytes.
 #include <math.h>
 
@@ -25,14 +26,17 @@ __global__ __launch_bounds__(kSigThreads) void kld_signal_kernel(
     int32_t *__restrict__ count, int32_t W, int32_t n_short, int32_t n_long, float delta, float eps,
     float *__restrict__ mu_last, float *__restrict__ var_short, float *__restrict__ var_long,
     float *__restrict__ wvir, float *__restrict__ sf, uint32_t *__restrict__ seq_err) {
+  const int32_t b = int32_t(blockIdx.x) * (kSigThreads / 64) + int32_t(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  // the ring state does not depend on the layout: fetch it with the layout check
+  RingPrefetch rp{};
+  if (b < B) rp = wave_ring_prefetch(hist + int64_t(b) * W, head + b, count + b, W);
   int bad = 0;
-  for (int32_t b = threadIdx.x; b < B; b += blockDim.x)
-    if (sl[b] < 0 || int64_t(cu_sl[b + 1]) - int64_t(cu_sl[b]) != int64_t(sl[b])) bad = 1;
+  for (int32_t q = threadIdx.x; q < B; q += blockDim.x)
+    if (sl[q] < 0 || int64_t(cu_sl[q + 1]) - int64_t(cu_sl[q]) != int64_t(sl[q])) bad = 1;
   bad = __syncthreads_or(bad);
   if (cu_sl[0] != 0 || int64_t(cu_sl[B]) != N) bad = 1;
-  const int32_t b = int32_t(blockIdx.x) * (kSigThreads / 64) + int32_t(threadIdx.x >> 6);
   if (b >= B) return;
-  const int lane = threadIdx.x & 63;
   if (bad) {
     if (lane == 0) {
       seq_err[b] = DSDE_ERR_LAYOUT;
@@ -40,8 +44,8 @@ __global__ __launch_bounds__(kSigThreads) void kld_signal_kernel(
     }
     return;
   }
-  const uint32_t e = wave_signal_update(sl[b], cu_sl[b], kld, 0.0f, hist + int64_t(b) * W, head + b, count + b, W,
-                                        n_short, n_long, delta, eps, mu_last + b, var_short + b, var_long + b,
+  const uint32_t e = wave_signal_update(sl[b], cu_sl[b], kld, 0.0f, rp, hist + int64_t(b) * W, head + b, count + b,
+                                        W, n_short, n_long, delta, eps, mu_last + b, var_short + b, var_long + b,
                                         wvir + b, sf + b);
   if (lane == 0) seq_err[b] = e;
 }
@@ -52,10 +56,10 @@ __global__ __launch_bounds__(kCapThreads) void next_sl_kernel(int32_t B, const f
                                                               int32_t sl_hi, float *__restrict__ sl_hat,
                                                               float *__restrict__ sl_cap,
                                                               int32_t *__restrict__ sl_next,
-                                                              uint32_t *__restrict__ seq_err) {
+                                                              uint32_t *__restrict__ seq_err, bool or_err) {
   __shared__ double red_s[kCapThreads];
   __shared__ int red_n[kCapThreads];
-  block_next_sl(B, sf, wvir, sl_max, sl_min, sl_hi, sl_hat, sl_cap, sl_next, seq_err, false, red_s, red_n);
+  block_next_sl(B, sf, wvir, sl_max, sl_min, sl_hi, sl_hat, sl_cap, sl_next, seq_err, or_err, red_s, red_n);
 }
 
 }  // namespace
@@ -73,10 +77,11 @@ int launch_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu
 }
 
 int launch_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max, float sl_min, int32_t sl_hi,
-                   float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err, hipStream_t stream) {
+                   float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err, bool or_err,
+                   hipStream_t stream) {
   (void)hipGetLastError();
   next_sl_kernel<<<dim3(1), dim3(kCapThreads), 0, stream>>>(B, sf, wvir, sl_max, sl_min, sl_hi, sl_hat, sl_cap,
-                                                            sl_next, seq_err);
+                                                            sl_next, seq_err, or_err);
   return hipGetLastError() == hipSuccess ? DSDE_OK : DSDE_DEVICE_ERROR;
 }
 

@@ -15,51 +15,126 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   return v;
 }
 
-// Recency-weighted mean and population variance of the n newest ring entries
-// (h_1 newest, whose value is passed as `h1`), alpha_i = delta^(i-1),
-// evaluated by one wavefront (lane i holds entries i, i + 64, ...).
-// Fixed-order sums: bitwise reproducible.
-__device__ inline void wave_window_stats(const float *ring, int32_t W, int32_t newest, float h1, int32_t n,
-                                         double delta, double *mean, double *var) {
+// Ring slots one wavefront keeps in registers: with W <= 64 * kRingRegs every
+// window entry is read from registers, larger rings are read from memory.
+constexpr int kRingRegs = 4;
+
+// The ring state of one sequence, fetched by one wavefront ahead of use:
+// head, count, and ring slot l + 64 k in lane l, register k.
+struct RingPrefetch {
+  int32_t head, count;
+  float slot[kRingRegs];
+};
+
+__device__ __forceinline__ RingPrefetch wave_ring_prefetch(const float *ring, const int32_t *head,
+                                                           const int32_t *count, int32_t W) {
   const int lane = threadIdx.x & 63;
-  if (n <= 0) {
-    *mean = 0.0;
-    *var = 0.0;
-    return;
+  RingPrefetch r;
+  r.head = *head;
+  r.count = *count;
+#pragma unroll
+  for (int k = 0; k < kRingRegs; ++k) {
+    const int32_t i = lane + 64 * k;
+    r.slot[k] = ring[i < W ? i : W - 1];  // clamped index: always in bounds (W >= 1)
   }
-  double sa = 0.0, sah = 0.0;
-  for (int32_t i = lane; i < n; i += 64) {
-    const double alpha = pow(delta, double(i));
-    const double h = i == 0 ? double(h1) : double(ring[(newest - i + W) % W]);
-    sa += alpha;
-    sah += alpha * h;
-  }
-  sa = wave_sum_f64(sa);
-  sah = wave_sum_f64(sah);
-  const double mu = sah / sa;
-  double sv = 0.0;
-  for (int32_t i = lane; i < n; i += 64) {
-    const double alpha = pow(delta, double(i));
-    const double d = (i == 0 ? double(h1) : double(ring[(newest - i + W) % W])) - mu;
-    sv += alpha * d * d;
-  }
-  sv = wave_sum_f64(sv);
-  *mean = mu;
-  *var = sv / sa;
+  return r;
 }
 
-// Signal update of one sequence by one wavefront.  The sequence's `s` KLD
-// values are kld[first .. first + s) or, when kld is null (s <= 64), the
-// per-lane values `lane_kld` (lane j holds position j).  Ring hist[0..W) with
-// head/count.  Returns the error bits (DSDE_ERR_STATE, DSDE_ERR_SIGNAL); on
-// error nothing is pushed and every output is NaN.
-__device__ inline uint32_t wave_signal_update(int32_t s, int64_t first, const float *kld, float lane_kld, float *ring,
-                                              int32_t *head, int32_t *count, int32_t W, int32_t n_short,
-                                              int32_t n_long, float delta, float eps, float *mu_last,
-                                              float *var_short, float *var_long, float *wvir, float *sf) {
+// Value of ring slot `slot` (0 <= slot < W), in every lane that asks.  Must be
+// reached by the whole wavefront (it shuffles when the ring is in registers).
+__device__ __forceinline__ float ring_slot(const RingPrefetch &rp, const float *ring, int32_t W, int32_t slot) {
+  if (W <= 64 * kRingRegs) {
+    float v = 0.f;
+#pragma unroll
+    for (int k = 0; k < kRingRegs; ++k) {
+      const float x = __shfl(rp.slot[k], slot & 63);
+      if ((slot >> 6) == k) v = x;
+    }
+    return v;
+  }
+  return ring[slot];
+}
+
+// delta^n for n >= 0 by binary powering (a few multiplications, no pow()).
+__device__ __forceinline__ double pow_int(double x, int32_t n) {
+  double r = 1.0;
+  while (n) {
+    if (n & 1) r *= x;
+    x *= x;
+    n >>= 1;
+  }
+  return r;
+}
+
+// Recency-weighted means and population variances (Eqs. 6-7) of the ns and
+// nl newest ring entries (ns <= nl), evaluated together by one wavefront:
+// entry i (i = 0 newest, value h1 passed in registers) sits in ring slot
+// (newest - i) mod W and has weight alpha = delta^i.  Lane l holds entries
+// l, l + 64, ...; fixed-order sums, bitwise reproducible.
+__device__ inline void wave_windows(const RingPrefetch &rp, const float *ring, int32_t W, int32_t newest, float h1,
+                                    int32_t ns, int32_t nl, double delta, double *ms, double *vs, double *ml,
+                                    double *vl) {
+  const int lane = threadIdx.x & 63;
+  const int32_t rounds = (nl + 63) / 64;
+  double sa_s = 0.0, sah_s = 0.0, sa_l = 0.0, sah_l = 0.0;
+  for (int32_t r = 0; r < rounds; ++r) {
+    const int32_t i = lane + 64 * r;
+    const int32_t slot = i < W ? (newest - i + W) % W : 0;
+    const float raw = ring_slot(rp, ring, W, slot);
+    if (i < nl) {
+      const double h = i == 0 ? double(h1) : double(raw);
+      const double a = pow_int(delta, i);
+      sa_l += a;
+      sah_l += a * h;
+      if (i < ns) {
+        sa_s += a;
+        sah_s += a * h;
+      }
+    }
+  }
+  sa_s = wave_sum_f64(sa_s);
+  sah_s = wave_sum_f64(sah_s);
+  sa_l = wave_sum_f64(sa_l);
+  sah_l = wave_sum_f64(sah_l);
+  const double mu_s = ns > 0 ? sah_s / sa_s : 0.0, mu_l = nl > 0 ? sah_l / sa_l : 0.0;
+  double sv_s = 0.0, sv_l = 0.0;
+  for (int32_t r = 0; r < rounds; ++r) {
+    const int32_t i = lane + 64 * r;
+    const int32_t slot = i < W ? (newest - i + W) % W : 0;
+    const float raw = ring_slot(rp, ring, W, slot);
+    if (i < nl) {
+      const double h = i == 0 ? double(h1) : double(raw);
+      const double a = pow_int(delta, i);
+      const double dl = h - mu_l;
+      sv_l += a * dl * dl;
+      if (i < ns) {
+        const double ds = h - mu_s;
+        sv_s += a * ds * ds;
+      }
+    }
+  }
+  sv_s = wave_sum_f64(sv_s);
+  sv_l = wave_sum_f64(sv_l);
+  *ms = mu_s;
+  *ml = mu_l;
+  *vs = ns > 0 ? sv_s / sa_s : 0.0;
+  *vl = nl > 0 ? sv_l / sa_l : 0.0;
+}
+
+// Signal update of one sequence by one wavefront (Sec. 3.1.2).  The sequence's
+// `s` KLD values are kld[first .. first + s) or, when kld is null (s <= 64),
+// the per-lane values `lane_kld` (lane j holds position j).  `rp` is the ring
+// state fetched by this wavefront; the ring is hist[0..W).  Returns the error
+// bits (DSDE_ERR_STATE, DSDE_ERR_SIGNAL); on error nothing is pushed and every
+// output is NaN.  Must be reached by the whole wavefront.
+__device__ inline uint32_t wave_signal_update(int32_t s, int64_t first, const float *kld, float lane_kld,
+                                              const RingPrefetch &rp, float *ring, int32_t *head, int32_t *count,
+                                              int32_t W, int32_t n_short, int32_t n_long, float delta, float eps,
+                                              float *mu_last, float *var_short, float *var_long, float *wvir,
+                                              float *sf) {
   const int lane = threadIdx.x & 63;
   uint32_t err = 0;
-  const int32_t hd = *head, cnt = *count;
+  const int32_t hd = rp.head, cnt = rp.count;
   if (hd < 0 || hd >= W || cnt < 0 || cnt > W) err |= DSDE_ERR_STATE;
   double mu = 0.0;
   if (!err && s > 0) {
@@ -78,20 +153,21 @@ __device__ inline uint32_t wave_signal_update(int32_t s, int64_t first, const fl
   }
   int32_t h = hd, c = cnt;
   float h1;
-  if (s > 0) {  // push the step's mean KLD; i = 1 is the step just verified
+  if (s > 0) {  // push the step's mean KLD; i = 0 is the step just verified
     h1 = float(mu);
-    // every lane reads the older entries before lane 0 overwrites the slot
-    // below; the pushed value itself is passed in registers
+    // the older entries are read before lane 0 overwrites the slot below; the
+    // pushed value itself is passed in registers
     h = (h + 1) % W;
     c = c < W ? c + 1 : W;
   } else {
-    h1 = c > 0 ? ring[(h - 1 + W) % W] : 0.0f;
+    const float newest_old = ring_slot(rp, ring, W, (h - 1 + W) % W);
+    h1 = c > 0 ? newest_old : 0.0f;
     mu = c > 0 ? double(h1) : 0.0;
   }
   const int32_t newest = (h - 1 + W) % W;
   double ms, vs, ml, vl;
-  wave_window_stats(ring, W, newest, h1, n_short < c ? n_short : c, double(delta), &ms, &vs);
-  wave_window_stats(ring, W, newest, h1, n_long < c ? n_long : c, double(delta), &ml, &vl);
+  wave_windows(rp, ring, W, newest, h1, n_short < c ? n_short : c, n_long < c ? n_long : c, double(delta), &ms, &vs,
+               &ml, &vl);
   if (s > 0 && lane == 0) {
     ring[newest] = h1;
     *head = h;

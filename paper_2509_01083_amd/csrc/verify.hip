@@ -27,6 +27,7 @@
 //                      batch cap and the next speculation lengths.
 //
 // Every reduction runs in a fixed order, so results are bitwise reproducible.
+#include <hip/hip_ext.h>
 #include <math.h>
 
 #include "common.hpp"
@@ -92,7 +93,6 @@ template <int DT, bool VEC>
 struct Layout;
 template <>
 struct Layout<DSDE_BF16, true> {
-  static constexpr int kVec = 8;
   __device__ static int64_t index(int64_t chunk, int i, int t) {
     return 8 * (chunk * 1024 + (i / 8) * 256 + t) + (i % 8);
   }
@@ -103,7 +103,6 @@ struct Layout<DSDE_BF16, true> {
 };
 template <>
 struct Layout<DSDE_FP32, true> {
-  static constexpr int kVec = 4;
   __device__ static int64_t index(int64_t chunk, int i, int t) {
     return 4 * (chunk * 2048 + (i / 4) * 256 + t) + (i % 4);
   }
@@ -114,7 +113,6 @@ struct Layout<DSDE_FP32, true> {
 };
 template <int DT>
 struct Layout<DT, false> {
-  static constexpr int kVec = 1;
   __device__ static int64_t index(int64_t chunk, int i, int t) { return chunk * kChunk + int64_t(i) * 256 + t; }
   __device__ static void owner(int64_t local, int *t, int *i) {
     *t = int(local & 255);
@@ -201,6 +199,50 @@ __device__ __forceinline__ void load_chunk_f32(const void *row, int64_t V, int64
 #pragma unroll
     for (int i = 0; i < kEltsPerThread; ++i) {
       const int64_t v = chunk * kChunk + int64_t(i) * 256 + t;
+      const float x = load_logit(row, DT, v < V ? v : V - 1);
+      z[i] = v < V ? x : kPadF32;
+    }
+  }
+}
+
+// R consecutive logits of a row, from `start` (a multiple of R, R a multiple
+// of 8), padded past V.
+template <int DT, bool VEC, int R>
+__device__ __forceinline__ void load_run(const void *row, int64_t V, int64_t start, float (&z)[R]) {
+  if constexpr (VEC && DT == DSDE_BF16) {
+    const uint4 *p = (const uint4 *)row;
+    const int64_t last = V / 8 - 1;
+#pragma unroll
+    for (int q = 0; q < R / 8; ++q) {
+      const int64_t i = start / 8 + q;
+      const uint4 a = p[min(i, last)];
+      const uint4 v = i <= last ? a : make_uint4(kPadBf16x2, kPadBf16x2, kPadBf16x2, kPadBf16x2);
+      z[8 * q + 0] = bf_lo(v.x);
+      z[8 * q + 1] = bf_hi(v.x);
+      z[8 * q + 2] = bf_lo(v.y);
+      z[8 * q + 3] = bf_hi(v.y);
+      z[8 * q + 4] = bf_lo(v.z);
+      z[8 * q + 5] = bf_hi(v.z);
+      z[8 * q + 6] = bf_lo(v.w);
+      z[8 * q + 7] = bf_hi(v.w);
+    }
+  } else if constexpr (VEC && DT == DSDE_FP32) {
+    const float4 *p = (const float4 *)row;
+    const int64_t last = V / 4 - 1;
+#pragma unroll
+    for (int q = 0; q < R / 4; ++q) {
+      const int64_t i = start / 4 + q;
+      const float4 a = p[min(i, last)];
+      const bool ok = i <= last;
+      z[4 * q + 0] = ok ? a.x : kPadF32;
+      z[4 * q + 1] = ok ? a.y : kPadF32;
+      z[4 * q + 2] = ok ? a.z : kPadF32;
+      z[4 * q + 3] = ok ? a.w : kPadF32;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const int64_t v = start + i;
       const float x = load_logit(row, DT, v < V ? v : V - 1);
       z[i] = v < V ? x : kPadF32;
     }
@@ -381,8 +423,18 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
 }
 
 // ---------------------------------------------------------------------------
-// acceptance (+ fused signal update)
+// per-sequence kernel: acceptance, draw weights and draw
 // ---------------------------------------------------------------------------
+
+constexpr int kSeqThreads = 512;              // 8 wavefronts per sequence
+constexpr int kSeqWaves = kSeqThreads / 64;
+constexpr int kVirt = kThreads / 64;          // chunk-layout threads played by one lane (4)
+constexpr int kSignalWave = 1;                // wavefront that runs the fused signal update
+
+// How many of a lane's chunk-layout threads one loop iteration handles: as
+// many as the registers allow loads in flight for.
+template <int DT, bool VEC>
+constexpr int kVirtUnroll = !VEC ? 1 : DT == DSDE_BF16 ? kVirt : 2;
 
 struct StepParams {
   const void *target, *draft;
@@ -396,8 +448,18 @@ struct StepParams {
   double *row_lse;
   const PairChunk *part;
   const Gathered *gathered;
-  DrawJob *jobs;
-  DrawChunk *dchunks;
+};
+
+// What the draw of one sequence needs, decided by the acceptance.
+struct DrawJob {
+  int32_t kind;          // 0: residual of the first rejected pair, 1: bonus row, -1: nothing (flagged)
+  int32_t accepted;      // a_b
+  int32_t target_row;
+  int32_t draft_row;     // -1 for the bonus row
+  float scale;           // c = log2(e) / T_b
+  float mt, md;          // row reference shifts of the rejected pair
+  float inv_sp, inv_sq;  // 1 / row sums of the rejected pair
+  float u;               // draw uniform
 };
 
 // xor-butterfly reductions inside aligned groups of G lanes (G a power of two)
@@ -423,7 +485,7 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
                                      int *st_bad) {
   constexpr int P = 64 / G;  // pairs per wavefront
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane % G;
-  for (int32_t base = 0; base < s; base += kWaves * P) {
+  for (int32_t base = 0; base < s; base += kSeqWaves * P) {
     const int32_t j = base + wave * P + lane / G;
     float lmt = -INFINITY, lmd = -INFINITY;
     double lsp = 0.0, lsq = 0.0, la = 0.0;
@@ -472,30 +534,166 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
   }
 }
 
-template <bool FUSED>
-__global__ __launch_bounds__(kThreads) void accept_kernel(const StepParams P, const SignalArgs S) {
+// Total of the residual weights max(0, p - q) over one chunk of the rejected
+// pair, by one wavefront (lane l plays the chunk-layout threads l + 64 k):
+// per-thread fp32 sums in slot order, one wave sum per k, then the four in
+// order in fp64.
+template <int DT, bool VEC>
+__device__ inline double residual_chunk(const char *trow, const char *drow, int64_t V, int64_t ch,
+                                        const DrawJob &job) {
+  const int lane = threadIdx.x & 63;
+  float sw[kVirt];
+#pragma unroll kVirtUnroll<DT, VEC>
+  for (int k = 0; k < kVirt; ++k) {
+    float zt[kEltsPerThread], zd[kEltsPerThread];
+    load_chunk_f32<DT, VEC>(trow, V, ch, lane + 64 * k, zt);
+    load_chunk_f32<DT, VEC>(drow, V, ch, lane + 64 * k, zd);
+    float a = 0.f;
+#pragma unroll
+    for (int i = 0; i < kEltsPerThread; ++i) {
+      // padding gives p = q = 0, hence zero weight
+      const float p = fast_exp2(fmaf(zt[i], job.scale, -job.mt)) * job.inv_sp;
+      const float q = fast_exp2(fmaf(zd[i], job.scale, -job.md)) * job.inv_sq;
+      a += fmaxf(p - q, 0.0f);
+    }
+    sw[k] = wave_sum(a);
+  }
+  double w = 0.0;
+#pragma unroll
+  for (int k = 0; k < kVirt; ++k) w += double(sw[k]);
+  return w;
+}
+
+// Total of p over one chunk of the rejected pair's target row (the draw's
+// fallback when the residual has no mass), in the same order.
+template <int DT, bool VEC>
+__device__ inline double target_p_chunk(const char *trow, int64_t V, int64_t ch, const DrawJob &job) {
+  const int lane = threadIdx.x & 63;
+  float sp[kVirt];
+#pragma unroll kVirtUnroll<DT, VEC>
+  for (int k = 0; k < kVirt; ++k) {
+    float zt[kEltsPerThread];
+    load_chunk_f32<DT, VEC>(trow, V, ch, lane + 64 * k, zt);
+    float b = 0.f;
+#pragma unroll
+    for (int i = 0; i < kEltsPerThread; ++i) b += fast_exp2(fmaf(zt[i], job.scale, -job.mt)) * job.inv_sp;
+    sp[k] = wave_sum(b);
+  }
+  double p = 0.0;
+#pragma unroll
+  for (int k = 0; k < kVirt; ++k) p += double(sp[k]);
+  return p;
+}
+
+// Bonus row, one chunk, by one wavefront: the chunk reference ref = max(z) c,
+// the total of 2^(z c - ref), and whether a NaN or +-inf logit was seen (+inf
+// shows in the max, NaN in the sum, -inf in the min; padding is finite).
+template <int DT, bool VEC>
+__device__ inline void bonus_chunk(const char *trow, int64_t V, int64_t ch, float scale, double *w_out,
+                                   float *ref_out, int *bad_out) {
+  const int lane = threadIdx.x & 63;
+  float m = -INFINITY, lo = INFINITY;
+  float sum[kVirt];
+  if constexpr (VEC && DT == DSDE_BF16) {
+    // one load: the raw chunk stays in registers for both passes
+    RawBf16 r[kVirt];
+#pragma unroll
+    for (int k = 0; k < kVirt; ++k) r[k] = load_raw_bf16(trow, V, ch, lane + 64 * k);
+#pragma unroll
+    for (int k = 0; k < kVirt; ++k)
+#pragma unroll
+      for (int i = 0; i < kEltsPerThread; ++i) {
+        const float z = pick_bf16(r[k], i);
+        m = fmaxf(m, z);
+        lo = fminf(lo, z);
+      }
+    const float ref = wave_max(m) * scale;
+#pragma unroll
+    for (int k = 0; k < kVirt; ++k) {
+      float a = 0.f;
+#pragma unroll
+      for (int i = 0; i < kEltsPerThread; ++i) a += fast_exp2(fmaf(pick_bf16(r[k], i), scale, -ref));
+      sum[k] = a;
+    }
+    *ref_out = ref;
+  } else {
+#pragma unroll kVirtUnroll<DT, VEC>
+    for (int k = 0; k < kVirt; ++k) {
+      float z[kEltsPerThread];
+      load_chunk_f32<DT, VEC>(trow, V, ch, lane + 64 * k, z);
+#pragma unroll
+      for (int i = 0; i < kEltsPerThread; ++i) {
+        m = fmaxf(m, z[i]);
+        lo = fminf(lo, z[i]);
+      }
+    }
+    const float ref = wave_max(m) * scale;
+    // second pass over the same logits (now in cache)
+#pragma unroll kVirtUnroll<DT, VEC>
+    for (int k = 0; k < kVirt; ++k) {
+      float z[kEltsPerThread];
+      load_chunk_f32<DT, VEC>(trow, V, ch, lane + 64 * k, z);
+      float a = 0.f;
+#pragma unroll
+      for (int i = 0; i < kEltsPerThread; ++i) a += fast_exp2(fmaf(z[i], scale, -ref));
+      sum[k] = a;
+    }
+    *ref_out = ref;
+  }
+  double w = 0.0;
+#pragma unroll
+  for (int k = 0; k < kVirt; ++k) w += double(wave_sum(sum[k]));
+  const int bad = __ballot(m == INFINITY || lo == -INFINITY) != 0;
+  *w_out = w;
+  *bad_out = bad || !isfinite(w) || !isfinite(*ref_out);
+}
+
+
+// One workgroup per sequence.
+//   1. all wavefronts: combine the chunk partials of the drafted pairs (fp64);
+//      wavefront 0: input checks, KLD, acceptance u < p(x)/q(x) (fp64), the
+//      accepted tokens and the draw job.
+//   2. wavefront w: the draw-weight totals of chunks w, w + 8, ... (residual
+//      max(0, p - q) of the first rejected pair, or the bonus row), into LDS.
+//   3. wavefront 0: fixed-order fp64 prefix over the chunk totals to the chunk
+//      holding u' * Z, then the ordered scan inside it.  Fused: wavefront 1
+//      meanwhile runs the signal update of the sequence.
+template <int DT, bool VEC, bool FUSED>
+__global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, const SignalArgs S) {
   __shared__ float st_mt[DSDE_MAX_K + 1], st_md[DSDE_MAX_K + 1];
   __shared__ double st_sp[DSDE_MAX_K + 1], st_sq[DSDE_MAX_K + 1], st_a[DSDE_MAX_K + 1];
   __shared__ int st_bad[DSDE_MAX_K + 1];
+  __shared__ float s_kld[64];
+  __shared__ double ch_w[kMaxChunks], ch_p[kMaxChunks];
+  __shared__ float ch_ref[kMaxChunks];
+  __shared__ int ch_bad[kMaxChunks];
+  __shared__ DrawJob s_job;
+  __shared__ int32_t s_chunk, s_mode, s_bad;
+  __shared__ double s_rem;
+  __shared__ float s_ref;
+  __shared__ double s_wave_total[kSeqWaves];
+  __shared__ int s_wave_cand[kSeqWaves];
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const int32_t b = blockIdx.x;
   const int32_t width = P.k_max + 1;
   int32_t *tok = P.tokens + int64_t(b) * width;
-  DrawJob none{};
-  none.kind = -1;
-  uint32_t err = P.seq_err[b];
+  // the signal wavefront fetches the ring state first: it does not depend on
+  // anything this kernel computes
+  RingPrefetch rp{};
+  if constexpr (FUSED)
+    if (wave == kSignalWave) rp = wave_ring_prefetch(S.hist + int64_t(b) * S.W, S.head + b, S.count + b, S.W);
+  uint32_t err = P.seq_err[b];  // the set-up's layout verdict
   if (err & DSDE_ERR_LAYOUT) {
     if (t < width) tok[t] = P.pad_id;
     if (t == 0) {
       P.accepted[b] = 0;
-      P.jobs[b] = none;
       if constexpr (FUSED) S.mu_last[b] = S.var_short[b] = S.var_long[b] = S.wvir[b] = S.sf[b] = NAN;
     }
     return;
   }
   const int32_t s = P.sl[b], first = P.cu_sl[b];
   const float T = P.temperature[b], ur = P.u_res[b];
-  // per-position inputs of wave 0 (lane j = drafted position j), fetched
+  // per-position inputs of wavefront 0 (lane j = drafted position j), fetched
   // together with the chunk partials below
   int32_t x = 0;
   float u = 0.f;
@@ -505,6 +703,8 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(const StepParams P, co
     u = P.u_acc[first + lane];
     gz = P.gathered[first + lane];
   }
+
+  // ---- 1. acceptance
   // row statistics of every drafted pair (read even for a flagged sequence:
   // the layout is valid, so every access stays in bounds)
   if (s > 0) {
@@ -516,235 +716,154 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(const StepParams P, co
       combine_pairs<64>(P.part, first, s, P.nc, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
   }
   __syncthreads();
-  if (wave != 0) return;
-  // per-sequence input checks
-  {
-    uint32_t e = 0;
-    if (lane < s) {
-      if (x < 0 || int64_t(x) >= P.V) e |= DSDE_ERR_TOKEN;
-      if (!(u >= 0.0f && u < 1.0f)) e |= DSDE_ERR_UNIFORM;
-    }
-    for (int32_t j = lane + 64; j < s; j += 64) {  // only when k_max > 63 would allow it
-      const int32_t xj = P.draft_tokens[first + j];
-      if (xj < 0 || int64_t(xj) >= P.V) e |= DSDE_ERR_TOKEN;
-    }
-    if (lane == 0) {
-      if (!(T >= kMinTemp && T <= kMaxTemp)) e |= DSDE_ERR_TEMP;
-      if (!(ur >= 0.0f && ur < 1.0f)) e |= DSDE_ERR_UNIFORM;
-    }
+  if (wave == 0) {
+    {  // per-sequence input checks
+      uint32_t e = 0;
+      if (lane < s) {
+        if (x < 0 || int64_t(x) >= P.V) e |= DSDE_ERR_TOKEN;
+        if (!(u >= 0.0f && u < 1.0f)) e |= DSDE_ERR_UNIFORM;
+      }
+      if (lane == 0) {
+        if (!(T >= kMinTemp && T <= kMaxTemp)) e |= DSDE_ERR_TEMP;
+        if (!(ur >= 0.0f && ur < 1.0f)) e |= DSDE_ERR_UNIFORM;
+      }
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) e |= __shfl_xor(e, o);
-    err |= e;
-  }
-  const float c = kLog2e / T;  // the same expression as the set-up's scale
-  const bool active = lane < s && !err;
-  bool ok = false, bad = false;
-  float my_kld = 0.f;
-  if (active) {
-    bad = st_bad[lane] != 0;
-    const double sp = st_sp[lane], sq = st_sq[lane];
-    const double l2sp = log2(sp), l2sq = log2(sq);
-    // KL in log2 units: E_p[(z_t c - mt) - (z_d c - md)] - log2 S_p + log2 S_q
-    const double kl = (st_a[lane] / sp - l2sp + l2sq) * kLn2;
-    my_kld = kl > 0.0 ? float(kl) : 0.0f;
-    // log2 p(x) - log2 q(x); z * c is exact in double
-    const double lr = (double(gz.zt) * double(c) - double(st_mt[lane]) - l2sp) -
-                      (double(gz.zd) * double(c) - double(st_md[lane]) - l2sq);
-    ok = double(u) < exp2(lr);
-    if (!bad && P.row_lse) {
-      P.row_lse[2 * (first + lane)] = (double(st_mt[lane]) + l2sp) * kLn2;
-      P.row_lse[2 * (first + lane) + 1] = (double(st_md[lane]) + l2sq) * kLn2;
+      for (int o = 32; o > 0; o >>= 1) e |= __shfl_xor(e, o);
+      err |= e;
     }
-  }
-  if (__ballot(bad)) err |= DSDE_ERR_LOGIT;
-  const uint64_t mask = __ballot(ok);
-  int32_t a = int32_t(__builtin_ctzll(~mask));
-  if (a > s) a = s;
-  if (err) {
-    a = 0;
-    my_kld = NAN;
-  }
-  if (lane < s) P.kld[first + lane] = my_kld;
-  if (lane < width) tok[lane] = lane < a ? x : P.pad_id;
-  if (lane == 0) {
-    P.accepted[b] = a;
-    DrawJob j = none;
-    if (!err) {
-      j.accepted = a;
-      j.scale = c;
-      j.u = ur;
-      if (a < s) {
-        j.kind = 0;
-        j.target_row = first + b + a;
-        j.draft_row = first + a;
-        j.mt = st_mt[a];
-        j.md = st_md[a];
-        j.inv_sp = float(1.0 / st_sp[a]);
-        j.inv_sq = float(1.0 / st_sq[a]);
-      } else {
-        j.kind = 1;
-        j.target_row = first + b + s;
-        j.draft_row = -1;
+    const float c = kLog2e / T;  // the same expression as the set-up's scale
+    const bool active = lane < s && !err;
+    bool ok = false, bad = false;
+    float my_kld = 0.f;
+    if (active) {
+      bad = st_bad[lane] != 0;
+      const double sp = st_sp[lane], sq = st_sq[lane];
+      const double l2sp = log2(sp), l2sq = log2(sq);
+      // KL in log2 units: E_p[(z_t c - mt) - (z_d c - md)] - log2 S_p + log2 S_q
+      const double kl = (st_a[lane] / sp - l2sp + l2sq) * kLn2;
+      my_kld = kl > 0.0 ? float(kl) : 0.0f;
+      // log2 p(x) - log2 q(x); z * c is exact in double
+      const double lr = (double(gz.zt) * double(c) - double(st_mt[lane]) - l2sp) -
+                        (double(gz.zd) * double(c) - double(st_md[lane]) - l2sq);
+      ok = double(u) < exp2(lr);
+      if (!bad && P.row_lse) {
+        P.row_lse[2 * (first + lane)] = (double(st_mt[lane]) + l2sp) * kLn2;
+        P.row_lse[2 * (first + lane) + 1] = (double(st_md[lane]) + l2sq) * kLn2;
       }
     }
-    P.jobs[b] = j;
-  }
-  if constexpr (FUSED) {
-    // the signal update of Sec. 3.1.2 on the KLD values just computed
-    err |= wave_signal_update(s, first, nullptr, my_kld, S.hist + int64_t(b) * S.W, S.head + b, S.count + b, S.W,
-                              S.n_short, S.n_long, S.delta, S.eps, S.mu_last + b, S.var_short + b, S.var_long + b,
-                              S.wvir + b, S.sf + b);
-  }
-  if (lane == 0) P.seq_err[b] = err;
-}
-
-// ---------------------------------------------------------------------------
-// draw chunk totals
-// ---------------------------------------------------------------------------
-
-template <int DT, bool VEC>
-__global__ __launch_bounds__(kThreads) void draw_chunk_kernel(const StepParams P) {
-  __shared__ float red[3][kWaves];
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  const int64_t unit = blockIdx.x;
-  const int32_t b = int32_t(unit / P.nc);
-  const int64_t chunk = unit - int64_t(b) * P.nc;
-  const DrawJob job = P.jobs[b];
-  if (job.kind < 0) return;
-  const size_t esz = DT == DSDE_BF16 ? 2 : 4;
-  const char *trow = (const char *)P.target + size_t(job.target_row) * size_t(P.V) * esz;
-  float zt[kEltsPerThread];
-  load_chunk_f32<DT, VEC>(trow, P.V, chunk, t, zt);
-  DrawChunk *out = P.dchunks + unit;
-  if (job.kind == 0) {
-    float zd[kEltsPerThread];
-    const char *drow = (const char *)P.draft + size_t(job.draft_row) * size_t(P.V) * esz;
-    load_chunk_f32<DT, VEC>(drow, P.V, chunk, t, zd);
-    float sw = 0.f, spp = 0.f;
-#pragma unroll
-    for (int i = 0; i < kEltsPerThread; ++i) {
-      // padding gives p = q = 0, hence zero weight
-      const float p = fast_exp2(fmaf(zt[i], job.scale, -job.mt)) * job.inv_sp;
-      const float q = fast_exp2(fmaf(zd[i], job.scale, -job.md)) * job.inv_sq;
-      sw += fmaxf(p - q, 0.0f);
-      spp += p;
+    if (__ballot(bad)) err |= DSDE_ERR_LOGIT;
+    const uint64_t mask = __ballot(ok);
+    int32_t a = int32_t(__builtin_ctzll(~mask));
+    if (a > s) a = s;
+    if (err) {
+      a = 0;
+      my_kld = NAN;
     }
-    sw = wave_sum(sw);
-    spp = wave_sum(spp);
+    if (lane < s) P.kld[first + lane] = my_kld;
+    s_kld[lane] = my_kld;
+    if (lane < width) tok[lane] = lane < a ? x : P.pad_id;
     if (lane == 0) {
-      red[0][wave] = sw;
-      red[1][wave] = spp;
+      P.accepted[b] = a;
+      DrawJob j{};
+      j.kind = -1;
+      if (!err) {
+        j.accepted = a;
+        j.scale = c;
+        j.u = ur;
+        if (a < s) {
+          j.kind = 0;
+          j.target_row = first + b + a;
+          j.draft_row = first + a;
+          j.mt = st_mt[a];
+          j.md = st_md[a];
+          j.inv_sp = float(1.0 / st_sp[a]);
+          j.inv_sq = float(1.0 / st_sq[a]);
+        } else {
+          j.kind = 1;
+          j.target_row = first + b + s;
+          j.draft_row = -1;
+        }
+      }
+      s_job = j;
+    }
+  }
+  __syncthreads();
+  const DrawJob job = s_job;
+
+  // ---- 2. draw-weight totals of every chunk
+  const size_t esz = DT == DSDE_BF16 ? 2 : 4;
+  const int32_t nc = P.nc;
+  if (job.kind >= 0) {
+    const char *trow = (const char *)P.target + size_t(job.target_row) * size_t(P.V) * esz;
+    if (job.kind == 0) {
+      const char *drow = (const char *)P.draft + size_t(job.draft_row) * size_t(P.V) * esz;
+      for (int32_t ch = wave; ch < nc; ch += kSeqWaves) {
+        const double w = residual_chunk<DT, VEC>(trow, drow, P.V, ch, job);
+        if (lane == 0) ch_w[ch] = w;
+      }
+    } else {
+      for (int32_t ch = wave; ch < nc; ch += kSeqWaves) {
+        double w;
+        float ref;
+        int bad;
+        bonus_chunk<DT, VEC>(trow, P.V, ch, job.scale, &w, &ref, &bad);
+        if (lane == 0) {
+          ch_w[ch] = w;
+          ch_ref[ch] = ref;
+          ch_bad[ch] = bad;
+        }
+      }
     }
     __syncthreads();
-    if (t == 0) {
-      DrawChunk dc{};
-      for (int w = 0; w < kWaves; ++w) {
-        dc.w += double(red[0][w]);
-        dc.p += double(red[1][w]);
+    if (job.kind == 0) {
+      // the residual's total mass, evaluated identically by every wavefront;
+      // without mass the draw falls back to p, whose chunk totals come next
+      double part = 0.0;
+      for (int32_t ch = lane; ch < nc; ch += 64) part += ch_w[ch];
+      if (!(wave_sum_f64(part) > 0.0)) {
+        for (int32_t ch = wave; ch < nc; ch += kSeqWaves) {
+          const double p = target_p_chunk<DT, VEC>(trow, P.V, ch, job);
+          if (lane == 0) ch_p[ch] = p;
+        }
+        __syncthreads();
       }
-      *out = dc;
     }
+  }
+
+  if constexpr (FUSED) {
+    if (wave == kSignalWave) {
+      // the signal update of Sec. 3.1.2 on the KLD values just computed
+      // (concurrent with the chunk search of wavefront 0)
+      const uint32_t e = wave_signal_update(s, first, nullptr, s_kld[lane], rp, S.hist + int64_t(b) * S.W,
+                                            S.head + b, S.count + b, S.W, S.n_short, S.n_long, S.delta, S.eps,
+                                            S.mu_last + b, S.var_short + b, S.var_long + b, S.wvir + b, S.sf + b);
+      if (e && lane == 0) atomicOr(&P.seq_err[b], e);
+    }
+  }
+  if (job.kind < 0) {
+    if (err && wave == 0 && lane == 0) atomicOr(&P.seq_err[b], err);
     return;
   }
-  // bonus row: chunk reference shift, and detection of non-finite logits
-  // (+inf shows in the max, NaN in the sum, -inf in the min)
-  float m = zt[0], lo = zt[0];
-#pragma unroll
-  for (int i = 1; i < kEltsPerThread; ++i) {
-    m = fmaxf(m, zt[i]);
-    if (Layout<DT, VEC>::index(chunk, i, t) < P.V) lo = fminf(lo, zt[i]);
-  }
-  int bad = (m == INFINITY || lo == -INFINITY) ? 1 : 0;
-  const float M = block_max(m, red[0]);
-  const float ref = M * job.scale;
-  float sum = 0.f;
-#pragma unroll
-  for (int i = 0; i < kEltsPerThread; ++i) sum += fast_exp2(fmaf(zt[i], job.scale, -ref));
-  sum = wave_sum(sum);
-  bad = __syncthreads_or(bad);
-  if (lane == 0) red[1][wave] = sum;
-  __syncthreads();
-  if (t == 0) {
-    DrawChunk dc{};
-    for (int w = 0; w < kWaves; ++w) dc.w += double(red[1][w]);
-    dc.ref = ref;
-    dc.bad = bad || !isfinite(dc.w) || !isfinite(ref);
-    *out = dc;
-  }
-}
 
-// ---------------------------------------------------------------------------
-// draw: locate u' * Z (+ fused batch cap)
-// ---------------------------------------------------------------------------
-
-// Exclusive block scan of one double per thread (fixed order); returns the
-// exclusive prefix and sets *total.
-__device__ double block_exclusive_scan(double v, double *lds, double *total) {
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  double incl = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const double y = __shfl_up(incl, o);
-    if (lane >= o) incl += y;
-  }
-  if (lane == 63) lds[wave] = incl;
-  __syncthreads();
-  double base = 0.0, all = 0.0;
-  for (int w = 0; w < kWaves; ++w) {
-    if (w < wave) base += lds[w];
-    all += lds[w];
-  }
-  __syncthreads();
-  *total = all;
-  return base + incl - v;
-}
-
-template <int DT, bool VEC, bool FUSED>
-__global__ __launch_bounds__(kThreads) void finish_kernel(const StepParams P, const SignalArgs S) {
-  constexpr int kv = Layout<DT, VEC>::kVec;
-  constexpr int kSlabs = kEltsPerThread / kv;
-  __shared__ double dsh[kWaves];
-  __shared__ double s_slab[kSlabs][kWaves];
-  __shared__ double s_rem;
-  __shared__ int64_t s_chunk;
-  __shared__ int s_mode, s_bad;
-  __shared__ float s_ref;
-  __shared__ unsigned long long s_y, s_last;
-  const int32_t b = blockIdx.x;
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  if constexpr (FUSED) {
-    if (b == P.B) {
-      __shared__ double red_s[kThreads];
-      __shared__ int red_n[kThreads];
-      block_next_sl(P.B, S.sf, S.wvir, S.sl_max, S.sl_min, S.sl_hi, S.sl_hat, S.sl_cap, S.sl_next, P.seq_err,
-                    true, red_s, red_n);
-      return;
-    }
-  }
-  const DrawJob job = P.jobs[b];
-  if (job.kind < 0) return;
-  const int32_t nc = P.nc;
-  const DrawChunk *dc = P.dchunks + int64_t(b) * nc;
-
-  // ---- the chunk holding u' * Z: wave 0, lanes over chunks, fixed-order fp64 sums
+  // ---- 3. the chunk holding u' * Z (wavefront 0, lanes over chunks, fixed-order fp64)
   if (wave == 0) {
     int mode = job.kind == 0 ? 0 : 2;  // 0: residual weights, 1: p of the rejected pair, 2: bonus exponentials
-    // lane l folds chunks l, l + 64, ... (in order) for its part of the prefix
     float ref_max = -INFINITY;
     int bad = 0;
     if (mode == 2) {
       for (int32_t ch = lane; ch < nc; ch += 64) {
-        bad |= dc[ch].bad;
-        ref_max = fmaxf(ref_max, dc[ch].ref);
+        bad |= ch_bad[ch];
+        ref_max = fmaxf(ref_max, ch_ref[ch]);
       }
       ref_max = wave_max(ref_max);
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) bad |= __shfl_xor(bad, o);
     }
     auto weight = [&](int32_t ch, int m) -> double {
-      return m == 0 ? dc[ch].w : m == 1 ? dc[ch].p : dc[ch].w * exp2(double(dc[ch].ref) - double(ref_max));
+      return m == 0 ? ch_w[ch] : m == 1 ? ch_p[ch] : ch_w[ch] * exp2(double(ch_ref[ch]) - double(ref_max));
     };
-    double Z = 0.0;
+    int32_t best = -1;
+    double best_excl = 0.0, Z = 0.0;
     if (!bad) {
       double part = 0.0;
       for (int32_t ch = lane; ch < nc; ch += 64) part += weight(ch, mode);
@@ -755,12 +874,12 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(const StepParams P, co
         for (int32_t ch = lane; ch < nc; ch += 64) part += weight(ch, 1);
         Z = wave_sum_f64(part);
       }
-    }
-    const double target_mass = double(job.u) * Z;
-    // walk 64 chunks at a time: inclusive wave scan, first chunk whose cumulative exceeds the target
-    int64_t found = nc - 1;
-    double before = 0.0, base = 0.0;
-    if (!bad) {
+      const double target_mass = double(job.u) * Z;
+      // inclusive scan 64 chunks at a time; the chunk holding the target is
+      // the last one with positive weight whose exclusive prefix is <= the
+      // target (prefixes tile exactly: each chunk's start is the previous
+      // chunk's end), which also covers rounding past the total
+      double base = 0.0;
       for (int32_t c0 = 0; c0 < nc; c0 += 64) {
         const int32_t ch = c0 + lane;
         const double w = ch < nc ? weight(ch, mode) : 0.0;
@@ -770,134 +889,124 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(const StepParams P, co
           const double y = __shfl_up(incl, o);
           if (lane >= o) incl += y;
         }
-        const uint64_t hit = __ballot(ch < nc && base + incl > target_mass);
-        if (hit) {
-          const int l = __builtin_ctzll(hit);
-          found = c0 + l;
-          before = base + __shfl(incl - w, l);
-          break;
+        incl = base + incl;
+        double excl = __shfl_up(incl, 1);
+        if (lane == 0) excl = base;
+        const uint64_t cand = __ballot(ch < nc && w > 0.0 && excl <= target_mass);
+        if (cand) {
+          const int l = 63 - __builtin_clzll(cand);
+          best = c0 + l;
+          best_excl = __shfl(excl, l);
         }
-        base += __shfl(incl, 63);
-        before = base;
+        base = __shfl(incl, 63);
+      }
+      if (lane == 0) {
+        const int32_t chunk = best >= 0 ? best : 0;
+        double rem = target_mass - best_excl;
+        if (rem < 0.0) rem = 0.0;
+        float ref = 0.f;
+        if (mode == 2) {
+          ref = ch_ref[chunk];
+          rem *= exp2(double(ref_max) - double(ref));  // into the chunk's own scale
+        }
+        s_chunk = chunk;
+        s_rem = rem;
+        s_ref = ref;
       }
     }
     if (lane == 0) {
-      double rem = target_mass - before;
-      if (rem < 0.0) rem = 0.0;
-      if (mode == 2 && !bad) rem *= exp2(double(ref_max) - double(dc[found].ref));  // into the chunk's own scale
-      s_rem = rem;
-      s_chunk = found;
       s_mode = mode;
       s_bad = bad;
-      s_ref = mode == 2 && !bad ? dc[found].ref : 0.f;
-      s_y = ~0ull;
-      s_last = 0;
     }
   }
   __syncthreads();
-  const int32_t width = P.k_max + 1;
   if (s_bad) {
     // a NaN or infinite logit in the bonus row: no token is emitted
-    if (t < width) P.tokens[int64_t(b) * width + t] = P.pad_id;
-    if (t == 0) {
-      P.accepted[b] = 0;
-      atomicOr(&P.seq_err[b], DSDE_ERR_LOGIT);
+    if (wave == 0) {
+      if (lane < width) tok[lane] = P.pad_id;
+      if (lane == 0) {
+        P.accepted[b] = 0;
+        atomicOr(&P.seq_err[b], err | DSDE_ERR_LOGIT);
+      }
     }
     return;
   }
 
-  // ---- the ordered scan inside that chunk
-  const size_t esz = DT == DSDE_BF16 ? 2 : 4;
-  const int64_t chunk = s_chunk;
+  // ---- 4. the ordered scan inside that chunk: thread t holds the 16
+  // consecutive logits from chunk * 8192 + 16 t; per-thread totals in token
+  // order, a block-wide inclusive scan, and the thread holding the target
+  // walks its own weights
   const int mode = s_mode;
-  const float c = job.scale, ref = s_ref;
+  const int64_t chunk = s_chunk;
+  const double rem = s_rem;
+  const float ref = s_ref;
   const char *trow = (const char *)P.target + size_t(job.target_row) * size_t(P.V) * esz;
-  float zt[kEltsPerThread], zd[kEltsPerThread];
-  load_chunk_f32<DT, VEC>(trow, P.V, chunk, t, zt);
-  if (mode != 2) {
-    const char *drow = (const char *)P.draft + size_t(job.draft_row) * size_t(P.V) * esz;
-    load_chunk_f32<DT, VEC>(drow, P.V, chunk, t, zd);
-  }
-  // weights of this thread's logits, computed exactly as for the chunk totals;
-  // slab g (ascending token order) holds slots [g*kv, (g+1)*kv) of every thread
-  float w[kEltsPerThread];
-  unsigned long long last = 0;  // 1 + index of the last positive weight
+  constexpr int kRun = kChunk / kSeqThreads;  // 16
+  const int64_t run0 = chunk * kChunk + int64_t(kRun) * t;
+  float w[kRun];
+  {
+    float zt[kRun];
+    load_run<DT, VEC, kRun>(trow, P.V, run0, zt);
+    if (mode == 0) {
+      float zd[kRun];
+      const char *drow = (const char *)P.draft + size_t(job.draft_row) * size_t(P.V) * esz;
+      load_run<DT, VEC, kRun>(drow, P.V, run0, zd);
 #pragma unroll
-  for (int i = 0; i < kEltsPerThread; ++i) {
-    float wi;
-    if (mode == 2) {
-      wi = fast_exp2(fmaf(zt[i], c, -ref));
+      for (int i = 0; i < kRun; ++i) {
+        const float p = fast_exp2(fmaf(zt[i], job.scale, -job.mt)) * job.inv_sp;
+        const float q = fast_exp2(fmaf(zd[i], job.scale, -job.md)) * job.inv_sq;
+        w[i] = fmaxf(p - q, 0.0f);
+      }
+    } else if (mode == 1) {
+#pragma unroll
+      for (int i = 0; i < kRun; ++i) w[i] = fast_exp2(fmaf(zt[i], job.scale, -job.mt)) * job.inv_sp;
     } else {
-      const float p = fast_exp2(fmaf(zt[i], c, -job.mt)) * job.inv_sp;
-      const float q = fast_exp2(fmaf(zd[i], c, -job.md)) * job.inv_sq;
-      wi = mode == 0 ? fmaxf(p - q, 0.0f) : p;
-    }
-    w[i] = wi;
-    if (wi > 0.0f) {
-      const unsigned long long idx = (unsigned long long)Layout<DT, VEC>::index(chunk, i, t) + 1;
-      last = idx > last ? idx : last;
+#pragma unroll
+      for (int i = 0; i < kRun; ++i) w[i] = fast_exp2(fmaf(zt[i], job.scale, -ref));
     }
   }
-  double tot[kSlabs];
+  double run_total = 0.0;
+  int last = -1;  // this thread's last positive weight
 #pragma unroll
-  for (int g = 0; g < kSlabs; ++g) {
-    double x = 0.0;
-#pragma unroll
-    for (int e = 0; e < kv; ++e) x += double(w[g * kv + e]);
-    tot[g] = x;
-    const double ws = wave_sum_f64(x);
-    if (lane == 0) s_slab[g][wave] = ws;
+  for (int i = 0; i < kRun; ++i) {
+    run_total += double(w[i]);
+    if (w[i] > 0.0f) last = i;
   }
+  double incl = run_total;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) s_wave_total[wave] = incl;
   __syncthreads();
-  // the slab that holds the remaining mass (every thread walks the same totals)
-  double rem = s_rem;
-  int gs = -1;
+  double base = 0.0;
+  for (int v = 0; v < wave; ++v) base += s_wave_total[v];
+  incl = base + incl;
+  double excl = __shfl_up(incl, 1);
+  if (lane == 0) excl = base;
+  // the thread holding the target: the last one with positive weight whose
+  // exclusive prefix is <= the target (rounding past the chunk's total lands
+  // on its last positive weight)
+  const uint64_t cand = __ballot(last >= 0 && excl <= rem);
+  if (lane == 0) s_wave_cand[wave] = cand ? 64 * wave + 63 - __builtin_clzll(cand) : -1;
+  __syncthreads();
+  int winner = -1;
 #pragma unroll
-  for (int g = 0; g < kSlabs; ++g) {
-    double st = 0.0;
+  for (int v = 0; v < kSeqWaves; ++v) winner = max(winner, s_wave_cand[v]);
+  if (t == (winner >= 0 ? winner : 0)) {
+    int pick = last >= 0 ? last : 0;
+    double acc = excl;
 #pragma unroll
-    for (int k = 0; k < kWaves; ++k) st += s_slab[g][k];
-    if (gs < 0) {
-      if (rem < st) {
-        gs = g;
-      } else {
-        rem -= st;
+    for (int i = 0; i < kRun; ++i) {
+      acc += double(w[i]);
+      if (acc > rem) {
+        pick = i;
+        break;
       }
     }
-  }
-  bool found = false;
-  if (gs >= 0) {
-    double x = 0.0;
-#pragma unroll
-    for (int g = 0; g < kSlabs; ++g)
-      if (g == gs) x = tot[g];
-    double slab_total;
-    const double excl = block_exclusive_scan(x, dsh, &slab_total);
-    if (rem >= excl && rem < excl + x) {
-      double acc = excl;
-      unsigned long long y = ~0ull;
-#pragma unroll
-      for (int g = 0; g < kSlabs; ++g)
-        if (g == gs) {
-#pragma unroll
-          for (int e = 0; e < kv; ++e) {
-            acc += double(w[g * kv + e]);
-            if (y == ~0ull && acc > rem) y = (unsigned long long)Layout<DT, VEC>::index(chunk, g * kv + e, t);
-          }
-        }
-      if (y != ~0ull) atomicMin(&s_y, y);
-    }
-    __syncthreads();
-    found = s_y != ~0ull;
-  }
-  if (!found) {
-    // rounding left u' * Z past this chunk's total: the last positive weight
-    atomicMax(&s_last, last);
-    __syncthreads();
-  }
-  if (t == 0) {
-    const unsigned long long y = found ? s_y : (s_last > 0 ? s_last - 1 : 0);
-    P.tokens[int64_t(b) * width + job.accepted] = int32_t(y);
+    tok[job.accepted] = int32_t(run0 + pick);
+    if (err) atomicOr(&P.seq_err[b], err);
   }
 }
 
@@ -906,16 +1015,25 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(const StepParams P, co
 static inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 template <int DT, bool VEC>
-static void launch_draw(const VerifyArgs &a, const StepParams &P, const SignalArgs &S, unsigned nc) {
-  draw_chunk_kernel<DT, VEC><<<dim3(unsigned(a.B) * nc), dim3(kThreads), 0, a.stream>>>(P);
+static void launch_seq(const VerifyArgs &a, const StepParams &P, const SignalArgs &S) {
   if (a.signal)
-    finish_kernel<DT, VEC, true><<<dim3(unsigned(a.B) + 1u), dim3(kThreads), 0, a.stream>>>(P, S);
+    seq_kernel<DT, VEC, true><<<dim3(unsigned(a.B)), dim3(kSeqThreads), 0, a.stream>>>(P, S);
   else
-    finish_kernel<DT, VEC, false><<<dim3(unsigned(a.B)), dim3(kThreads), 0, a.stream>>>(P, S);
+    seq_kernel<DT, VEC, false><<<dim3(unsigned(a.B)), dim3(kSeqThreads), 0, a.stream>>>(P, S);
+}
+
+// The statistics pass; with profiling events set, the events are attached to
+// the dispatch itself (they time exactly this kernel).
+template <typename K, typename... Args>
+static void launch_stats(K kernel, dim3 grid, const VerifyArgs &a, Args... args) {
+  if (a.prof_start && a.prof_stop)
+    hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, a.stream, a.prof_start, a.prof_stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, a.stream, args...);
 }
 
 int launch_verify(const VerifyArgs &a) {
-  const WorkspaceLayout L = workspace_layout(a.B, a.N, a.V);
+  const WorkspaceLayout L = workspace_layout(a.N, a.V);
   const int32_t nc = int32_t(num_chunks(a.V));
   char *ws = (char *)a.workspace;
   WorkItem *work = (WorkItem *)(ws + L.work);
@@ -928,22 +1046,20 @@ int launch_verify(const VerifyArgs &a) {
                    (a.dtype == DSDE_BF16 ? a.V % 8 == 0 : a.V % 4 == 0);
   if (a.N > 0) {
     const dim3 grid(unsigned(a.N * nc));
-    if (a.prof_start) (void)hipEventRecord(a.prof_start, a.stream);
+    const void *T = a.target, *D = a.draft;
+    const int64_t V = a.V;
+    const int32_t *tokens = a.draft_tokens;
     if (a.dtype == DSDE_BF16 && vec)
-      stats_kernel_bf16<<<grid, dim3(kThreads), 0, a.stream>>>(a.target, a.draft, a.V, nc, work, a.draft_tokens,
-                                                               part, gath);
+      launch_stats(stats_kernel_bf16, grid, a, T, D, V, nc, (const WorkItem *)work, tokens, part, gath);
     else if (a.dtype == DSDE_BF16)
-      stats_kernel_generic<DSDE_BF16, false><<<grid, dim3(kThreads), 0, a.stream>>>(a.target, a.draft, a.V, nc,
-                                                                                   work, a.draft_tokens, part,
-                                                                                   gath);
+      launch_stats(stats_kernel_generic<DSDE_BF16, false>, grid, a, T, D, V, nc, (const WorkItem *)work, tokens,
+                   part, gath);
     else if (vec)
-      stats_kernel_generic<DSDE_FP32, true><<<grid, dim3(kThreads), 0, a.stream>>>(a.target, a.draft, a.V, nc,
-                                                                                  work, a.draft_tokens, part, gath);
+      launch_stats(stats_kernel_generic<DSDE_FP32, true>, grid, a, T, D, V, nc, (const WorkItem *)work, tokens,
+                   part, gath);
     else
-      stats_kernel_generic<DSDE_FP32, false><<<grid, dim3(kThreads), 0, a.stream>>>(a.target, a.draft, a.V, nc,
-                                                                                   work, a.draft_tokens, part,
-                                                                                   gath);
-    if (a.prof_stop) (void)hipEventRecord(a.prof_stop, a.stream);
+      launch_stats(stats_kernel_generic<DSDE_FP32, false>, grid, a, T, D, V, nc, (const WorkItem *)work, tokens,
+                   part, gath);
   }
   StepParams P;
   P.target = a.target;
@@ -966,25 +1082,23 @@ int launch_verify(const VerifyArgs &a) {
   P.row_lse = a.row_lse;
   P.part = part;
   P.gathered = gath;
-  P.jobs = (DrawJob *)(ws + L.draw_job);
-  P.dchunks = (DrawChunk *)(ws + L.draw_chunk);
   const SignalArgs S = a.signal ? *a.signal : SignalArgs{};
-  if (a.signal)
-    accept_kernel<true><<<dim3(unsigned(a.B)), dim3(kThreads), 0, a.stream>>>(P, S);
-  else
-    accept_kernel<false><<<dim3(unsigned(a.B)), dim3(kThreads), 0, a.stream>>>(P, S);
   if (a.dtype == DSDE_BF16) {
     if (vec)
-      launch_draw<DSDE_BF16, true>(a, P, S, unsigned(nc));
+      launch_seq<DSDE_BF16, true>(a, P, S);
     else
-      launch_draw<DSDE_BF16, false>(a, P, S, unsigned(nc));
+      launch_seq<DSDE_BF16, false>(a, P, S);
   } else {
     if (vec)
-      launch_draw<DSDE_FP32, true>(a, P, S, unsigned(nc));
+      launch_seq<DSDE_FP32, true>(a, P, S);
     else
-      launch_draw<DSDE_FP32, false>(a, P, S, unsigned(nc));
+      launch_seq<DSDE_FP32, false>(a, P, S);
   }
-  return hipGetLastError() == hipSuccess ? DSDE_OK : DSDE_DEVICE_ERROR;
+  if (hipGetLastError() != hipSuccess) return DSDE_DEVICE_ERROR;
+  if (a.signal)
+    return launch_next_sl(a.B, S.sf, S.wvir, S.sl_max, S.sl_min, S.sl_hi, S.sl_hat, S.sl_cap, S.sl_next, a.seq_err,
+                          true, a.stream);
+  return DSDE_OK;
 }
 
 }  // namespace dsde

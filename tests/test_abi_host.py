@@ -52,8 +52,9 @@ def test_workspace_sizes(lib):
     ws = lib.dsde_verify_workspace_bytes
     assert ws(256, 1152, 128256, 8) > 0
     assert ws(256, 1152, 128256, 8) >= ws(256, 100, 128256, 8)
-    for bad in ((0, 0, 10, 4), (4, -1, 10, 4), (4, 0, 0, 4), (4, 0, 1 << 31, 4), (4, 0, 10, -1),
-                (4, 0, 10, 64), (4, 17, 10, 4)):
+    assert ws(4, 8, 4194304, 4) > 0  # the largest vocabulary (DSDE_MAX_VOCAB)
+    for bad in ((0, 0, 10, 4), (4, -1, 10, 4), (4, 0, 0, 4), (4, 0, 4194305, 4), (4, 0, 1 << 31, 4),
+                (4, 0, 10, -1), (4, 0, 10, 64), (4, 17, 10, 4)):
         assert ws(*bad) == 0, bad
 
 
@@ -69,7 +70,7 @@ def verify_args(**over):
 
 
 @pytest.mark.parametrize("over", [
-    dict(dtype=2), dict(dtype=-1), dict(V=0), dict(V=1 << 31), dict(B=0), dict(N=-1), dict(k_max=-1),
+    dict(dtype=2), dict(dtype=-1), dict(V=0), dict(V=4194305), dict(V=1 << 31), dict(B=0), dict(N=-1), dict(k_max=-1),
     dict(k_max=64), dict(N=17), dict(target=None), dict(sl=None), dict(cu_sl=None), dict(temp=None),
     dict(u_res=None), dict(acc=None), dict(tokens=None), dict(err=None), dict(ws=None), dict(draft=None),
     dict(toks=None), dict(u_acc=None), dict(kld=None), dict(ws=ctypes.c_void_p(0x1001)),

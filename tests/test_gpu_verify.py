@@ -69,6 +69,18 @@ def test_vocab_edges(gpu_lib, V, dtype):
     check_step(gpu_lib, step, f"vocab V={V} {dtype}")
 
 
+@pytest.mark.parametrize("V,dtype", [(600000, "bf16"), (600001, "bf16"), (600000, "fp32"), (4194304, "bf16")])
+def test_large_vocab(gpu_lib, V, dtype):
+    """More than 64 chunks per row (two rounds of the chunk walk, several chunks
+    per combining lane) up to the largest supported vocabulary."""
+    rng = np.random.default_rng(V % 1000 + 17)
+    sls = [3, 0, 2, 1] if V < 4194304 else [1, 1]
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V, noise=0.3)
+    temps = [1.0, 0.8, 1.1, 0.6][:len(sls)]
+    step = step_from_arrays(target, draft, sls, tokens, temps, u_acc, u_res, 3, dtype)
+    check_step(gpu_lib, step, f"large vocab V={V} {dtype}")
+
+
 def test_nothing_drafted(gpu_lib):
     rng = np.random.default_rng(3)
     V = 5000
