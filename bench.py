@@ -30,8 +30,8 @@ PEAK_HBM_GBPS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="b256")
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU time of the oracle baseline")
@@ -39,7 +39,7 @@ def parse():
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM traffic of the row-statistics kernel (from rocprofv3 counters)")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="also run a plain device copy of known size (for scaling the counters)")
+                    help="also run a streaming kernel of known size (for scaling the HBM counters)")
     return ap.parse_args()
 
 
@@ -54,6 +54,7 @@ def main():
 
     import paper_2509_01083_amd as dsde
     import workloads as W
+    from paper_2509_01083_amd.profiling import kernel_source_hash
 
     dsde.load()
     dev = torch.device("cuda:0")
@@ -88,10 +89,11 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
-    # second timed region of K steps whose row-statistics kernel carries a pair
-    # of HIP events attached to its dispatch (they time that kernel alone);
-    # kept apart from the headline region in case the events cost stream time.
-    # The events skip the system-scope fence of an ordinary event record.
+    # second timed region of K steps in which the library attaches a pair of
+    # HIP events to the completions of the set-up and row-statistics
+    # dispatches (the interval is the statistics kernel alone); kept apart
+    # from the headline region in case the events cost stream time.  The
+    # events skip the system-scope fence of an ordinary event record.
     ev = [(HipEvent(), HipEvent()) for _ in range(args.steps)]
     ev_region = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
     torch.cuda.synchronize()
@@ -123,7 +125,7 @@ def main():
     if os.path.exists(args.traffic):
         with open(args.traffic) as f:
             tr = json.load(f)
-        if tr.get("workload") == args.workload and tr.get("kernel_source_hash") == kernel_hash():
+        if tr.get("workload") == args.workload and tr.get("kernel_source_hash") == kernel_source_hash():
             traffic = tr.get("bytes_per_launch")
 
     result = {
@@ -155,13 +157,16 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"], result["parity"] = cpu_baseline(copies[last], outs[last], st, args.cpu_seconds)
     if args.copy_calibration:
-        n = 1 << 30
-        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        # a plain streaming kernel of known size for scaling the HBM counters:
+        # bitwise_not over 2^28 int32 reads 1 GiB and writes 1 GiB
+        n = 1 << 28
+        src = torch.zeros(n, dtype=torch.int32, device=dev)
         dst = torch.empty_like(src)
         for _ in range(3):
-            dst.copy_(src)
+            torch.bitwise_not(src, out=dst)
         torch.cuda.synchronize()
-        result["copy_calibration_bytes"] = n
+        result["copy_calibration"] = {"kernel": "bitwise_not", "read_bytes": 4 * n, "write_bytes": 4 * n,
+                                      "launches": 3}
     print(json.dumps(result), flush=True)
 
 
@@ -196,15 +201,6 @@ class HipEvent:
 
     def destroy(self):
         HipEvent._hip.hipEventDestroy(self.handle)
-
-
-def kernel_hash():
-    import hashlib
-    h = hashlib.sha256()
-    for f in ("verify.hip", "common.hpp"):
-        with open(os.path.join(ROOT, "paper_2509_01083_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
 
 
 def cpu_baseline(step, out, st, seconds):

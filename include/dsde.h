@@ -200,10 +200,13 @@ int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t d
 
 /*
  * Profiling hook: when both events are non-NULL (hipEvent_t, created with
- * timing enabled), every later dsde_verify or dsde_step with N > 0 launches its
- * row statistics kernel (the pass that reads every drafted row pair once) with
- * the two events attached to the dispatch itself, so that the elapsed time
- * between them is that kernel's execution time.  Passing NULLs turns it off.  Process-wide; not thread-safe.
+ * timing enabled), every later dsde_verify or dsde_step with N > 0 attaches
+ * `start` to the completion of its set-up kernel and `stop` to the completion
+ * of its row statistics kernel (the pass that reads every drafted row pair
+ * once), which runs right after it on the same stream; the elapsed time
+ * between them is that kernel's execution time.  Events created with
+ * hipEventDisableSystemFence add no gap to the stream.  Passing NULLs turns it
+ * off.  Process-wide; not thread-safe.
  */
 int32_t dsde_set_profile_events(void *start, void *stop);
 

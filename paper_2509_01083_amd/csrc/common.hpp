@@ -107,6 +107,10 @@ struct VerifyArgs {
 };
 
 int launch_verify(const VerifyArgs &a);
+// The set-up and statistics kernels of one verification step (stats.hip).
+void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gathered *gath);
+// Rows are 16-byte aligned and V a multiple of the vector width.
+bool rows_vectorizable(const VerifyArgs &a);
 int launch_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu_sl, const float *kld,
                       float *hist, int32_t *head, int32_t *count, int32_t W, int32_t n_short, int32_t n_long,
                       float delta, float eps, float *mu_last, float *var_short, float *var_long, float *wvir,

@@ -1,0 +1,225 @@
+// Device helpers shared by the row kernels: bf16/fp32 logit loads in the
+// chunk layouts, padding, and wavefront/workgroup reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace dsde {
+
+// bf16 -2^96: padding for logits past V.  It is below every admissible logit
+// (|z| <= 2^64), its exponential is exactly 0, and differences of two padding
+// values stay finite, so padding adds exactly nothing to any sum.
+constexpr uint32_t kPadBf16x2 = 0xef80ef80u;
+constexpr float kPadF32 = -7.9228162514264337593543950336e28f;  // -2^96
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// 2^x on the transcendental unit (about 1 ulp; results below 2^-126 flush to 0).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ float load_logit(const void *base, int dtype, int64_t idx) {
+  if (dtype == DSDE_BF16) return __uint_as_float(uint32_t(((const uint16_t *)base)[idx]) << 16);
+  return ((const float *)base)[idx];
+}
+
+// Block-wide max of one value per thread (all threads receive it).
+__device__ __forceinline__ float block_max(float v, float *lds) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  v = wave_max(v);
+  if (lane == 0) lds[wave] = v;
+  __syncthreads();
+  float m = lds[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) m = fmaxf(m, lds[w]);
+  __syncthreads();
+  return m;
+}
+
+// ---------------------------------------------------------------------------
+// chunk of a row held by one workgroup
+// ---------------------------------------------------------------------------
+//
+// The 8192 logits of chunk k of a row are spread over the 256 threads so that
+// each wavefront load is contiguous.  Thread t owns slots i = 0..31:
+//   bf16, 16-byte rows : logit 8 * (1024 k + 256 (i / 8) + t) + i % 8  (4 x uint4)
+//   fp32, 16-byte rows : logit 4 * (2048 k + 256 (i / 4) + t) + i % 4  (8 x float4)
+//   any other row      : logit 8192 k + 256 i + t                       (32 scalars)
+// Every load uses an in-bounds (clamped) index and the value is replaced by
+// padding past V, so the loads never branch.
+
+template <int DT, bool VEC>
+struct Layout;
+template <>
+struct Layout<DSDE_BF16, true> {
+  __device__ static int64_t index(int64_t chunk, int i, int t) {
+    return 8 * (chunk * 1024 + (i / 8) * 256 + t) + (i % 8);
+  }
+  __device__ static void owner(int64_t local, int *t, int *i) {
+    *t = int((local >> 3) & 255);
+    *i = int((local >> 11) * 8 + (local & 7));
+  }
+};
+template <>
+struct Layout<DSDE_FP32, true> {
+  __device__ static int64_t index(int64_t chunk, int i, int t) {
+    return 4 * (chunk * 2048 + (i / 4) * 256 + t) + (i % 4);
+  }
+  __device__ static void owner(int64_t local, int *t, int *i) {
+    *t = int((local >> 2) & 255);
+    *i = int((local >> 10) * 4 + (local & 3));
+  }
+};
+template <int DT>
+struct Layout<DT, false> {
+  __device__ static int64_t index(int64_t chunk, int i, int t) { return chunk * kChunk + int64_t(i) * 256 + t; }
+  __device__ static void owner(int64_t local, int *t, int *i) {
+    *t = int(local & 255);
+    *i = int(local >> 8);
+  }
+};
+
+// Raw bf16 chunk of one row: 4 x uint4 per thread.
+struct RawBf16 {
+  uint4 v0, v1, v2, v3;
+};
+
+__device__ __forceinline__ RawBf16 load_raw_bf16(const void *row, int64_t V, int64_t chunk, int t) {
+  const uint4 *p = (const uint4 *)row;
+  const int64_t last = V / 8 - 1;
+  const int64_t i0 = chunk * 1024 + t;
+  const uint4 pad = make_uint4(kPadBf16x2, kPadBf16x2, kPadBf16x2, kPadBf16x2);
+  const uint4 a0 = p[min(i0, last)], a1 = p[min(i0 + 256, last)];
+  const uint4 a2 = p[min(i0 + 512, last)], a3 = p[min(i0 + 768, last)];
+  RawBf16 r;
+  r.v0 = i0 <= last ? a0 : pad;
+  r.v1 = i0 + 256 <= last ? a1 : pad;
+  r.v2 = i0 + 512 <= last ? a2 : pad;
+  r.v3 = i0 + 768 <= last ? a3 : pad;
+  return r;
+}
+
+__device__ __forceinline__ float max2(uint32_t w) { return fmaxf(bf_lo(w), bf_hi(w)); }
+__device__ __forceinline__ float vmax(uint4 v) {
+  return fmaxf(fmaxf(max2(v.x), max2(v.y)), fmaxf(max2(v.z), max2(v.w)));
+}
+__device__ __forceinline__ float raw_max(const RawBf16 &r) {
+  return fmaxf(fmaxf(vmax(r.v0), vmax(r.v1)), fmaxf(vmax(r.v2), vmax(r.v3)));
+}
+__device__ __forceinline__ float pick_bf16(const RawBf16 &r, int i) {
+  const uint4 v = (i >> 3) == 0 ? r.v0 : (i >> 3) == 1 ? r.v1 : (i >> 3) == 2 ? r.v2 : r.v3;
+  const int w = (i >> 1) & 3;
+  const uint32_t x = w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
+  return (i & 1) ? bf_hi(x) : bf_lo(x);
+}
+
+// Statistics of one logit pair with references rt, rd (log2 domain).
+__device__ __forceinline__ void acc_pair(float zt, float zd, float c, float rt, float rd, float &sp, float &sq,
+                                         float &a) {
+  const float at = fmaf(zt, c, -rt), ad = fmaf(zd, c, -rd);
+  const float et = fast_exp2(at), ed = fast_exp2(ad);
+  sp += et;
+  sq += ed;
+  a = fmaf(et, at - ad, a);
+}
+__device__ __forceinline__ void acc_word(uint32_t t, uint32_t d, float c, float rt, float rd, float (&s)[6]) {
+  acc_pair(bf_lo(t), bf_lo(d), c, rt, rd, s[0], s[1], s[2]);
+  acc_pair(bf_hi(t), bf_hi(d), c, rt, rd, s[3], s[4], s[5]);
+}
+__device__ __forceinline__ void acc_vec(uint4 t, uint4 d, float c, float rt, float rd, float (&s)[6]) {
+  acc_word(t.x, d.x, c, rt, rd, s);
+  acc_word(t.y, d.y, c, rt, rd, s);
+  acc_word(t.z, d.z, c, rt, rd, s);
+  acc_word(t.w, d.w, c, rt, rd, s);
+}
+
+// Generic chunk of one row as 32 floats (fp32 rows, or rows without 16-byte alignment).
+template <int DT, bool VEC>
+__device__ __forceinline__ void load_chunk_f32(const void *row, int64_t V, int64_t chunk, int t,
+                                               float (&z)[kEltsPerThread]) {
+  if constexpr (VEC && DT == DSDE_FP32) {
+    const float4 *p = (const float4 *)row;
+    const int64_t last = V / 4 - 1;
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      const int64_t i = chunk * 2048 + g * 256 + t;
+      const float4 w = p[min(i, last)];
+      const bool ok = i <= last;
+      z[g * 4 + 0] = ok ? w.x : kPadF32;
+      z[g * 4 + 1] = ok ? w.y : kPadF32;
+      z[g * 4 + 2] = ok ? w.z : kPadF32;
+      z[g * 4 + 3] = ok ? w.w : kPadF32;
+    }
+  } else if constexpr (VEC && DT == DSDE_BF16) {
+    const RawBf16 r = load_raw_bf16(row, V, chunk, t);
+#pragma unroll
+    for (int i = 0; i < kEltsPerThread; ++i) z[i] = pick_bf16(r, i);
+  } else {
+#pragma unroll
+    for (int i = 0; i < kEltsPerThread; ++i) {
+      const int64_t v = chunk * kChunk + int64_t(i) * 256 + t;
+      const float x = load_logit(row, DT, v < V ? v : V - 1);
+      z[i] = v < V ? x : kPadF32;
+    }
+  }
+}
+
+// R consecutive logits of a row, from `start` (a multiple of R, R a multiple
+// of 8), padded past V.
+template <int DT, bool VEC, int R>
+__device__ __forceinline__ void load_run(const void *row, int64_t V, int64_t start, float (&z)[R]) {
+  if constexpr (VEC && DT == DSDE_BF16) {
+    const uint4 *p = (const uint4 *)row;
+    const int64_t last = V / 8 - 1;
+#pragma unroll
+    for (int q = 0; q < R / 8; ++q) {
+      const int64_t i = start / 8 + q;
+      const uint4 a = p[min(i, last)];
+      const uint4 v = i <= last ? a : make_uint4(kPadBf16x2, kPadBf16x2, kPadBf16x2, kPadBf16x2);
+      z[8 * q + 0] = bf_lo(v.x);
+      z[8 * q + 1] = bf_hi(v.x);
+      z[8 * q + 2] = bf_lo(v.y);
+      z[8 * q + 3] = bf_hi(v.y);
+      z[8 * q + 4] = bf_lo(v.z);
+      z[8 * q + 5] = bf_hi(v.z);
+      z[8 * q + 6] = bf_lo(v.w);
+      z[8 * q + 7] = bf_hi(v.w);
+    }
+  } else if constexpr (VEC && DT == DSDE_FP32) {
+    const float4 *p = (const float4 *)row;
+    const int64_t last = V / 4 - 1;
+#pragma unroll
+    for (int q = 0; q < R / 4; ++q) {
+      const int64_t i = start / 4 + q;
+      const float4 a = p[min(i, last)];
+      const bool ok = i <= last;
+      z[4 * q + 0] = ok ? a.x : kPadF32;
+      z[4 * q + 1] = ok ? a.y : kPadF32;
+      z[4 * q + 2] = ok ? a.z : kPadF32;
+      z[4 * q + 3] = ok ? a.w : kPadF32;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const int64_t v = start + i;
+      const float x = load_logit(row, DT, v < V ? v : V - 1);
+      z[i] = v < V ? x : kPadF32;
+    }
+  }
+}
+
+}  // namespace dsde

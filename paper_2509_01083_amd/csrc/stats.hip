@@ -1,0 +1,239 @@
+// The row-statistics pass of the verification step: one workgroup per
+// (drafted row pair, 8192-logit chunk) reads the chunk of the target and
+// draft rows once and writes max-shifted exponential sums of p and q and the
+// KL accumulator (Sec. 3.1.2), and captures the two logits at the drafted
+// token.  It carries almost all HBM bytes of the step.  A one-workgroup
+// set-up kernel before it validates the packed layout (Sec. 3.2) and writes
+// the work list (target row and scale of every drafted pair, in sequence
+// order).
+#include <hip/hip_ext.h>
+#include <math.h>
+
+#include "common.hpp"
+#include "row_io.hpp"
+
+namespace dsde {
+namespace {
+
+// ---------------------------------------------------------------------------
+// set-up
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(1024) void setup_kernel(int32_t B, int64_t N, int32_t k_max,
+                                                     const int32_t *__restrict__ sl,
+                                                     const int32_t *__restrict__ cu_sl,
+                                                     const float *__restrict__ temperature,
+                                                     uint32_t *__restrict__ seq_err, WorkItem *__restrict__ work) {
+  const int t = threadIdx.x;
+  const int64_t c_first = cu_sl[0], c_last = cu_sl[B];
+  int bad = 0;
+  for (int32_t b = t; b < B; b += blockDim.x) {
+    const int64_t s = sl[b];
+    if (s < 0 || s > k_max || int64_t(cu_sl[b + 1]) - int64_t(cu_sl[b]) != s) bad = 1;
+  }
+  bad = __syncthreads_or(bad);
+  if (c_first != 0 || c_last != N) bad = 1;
+  if (bad) {
+    for (int32_t b = t; b < B; b += blockDim.x) seq_err[b] = DSDE_ERR_LAYOUT;
+    for (int64_t k = t; k < N; k += blockDim.x) work[k] = WorkItem{int32_t(k), -1, 0u, 0};
+    return;
+  }
+  for (int32_t b = t; b < B; b += blockDim.x) {
+    const int32_t first = cu_sl[b], s = sl[b];
+    seq_err[b] = 0u;
+    // the same expression as every later kernel's scale; a temperature outside
+    // the admissible range is flagged by the acceptance kernel
+    const uint32_t cbits = __float_as_uint(kLog2e / temperature[b]);
+    for (int32_t j = 0; j < s; ++j) work[first + j] = WorkItem{first + j, first + b + j, cbits, 0};
+  }
+}
+
+// ---------------------------------------------------------------------------
+// row statistics of every drafted pair
+// ---------------------------------------------------------------------------
+
+// Chunk sums of one workgroup -> one PairChunk (fixed order: lanes, then waves in fp64).
+__device__ __forceinline__ void write_pair_chunk(float rt, float rd, float sp, float sq, float a, float (*red)[kWaves],
+                                                 PairChunk *out) {
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  sp = wave_sum(sp);
+  sq = wave_sum(sq);
+  a = wave_sum(a);
+  if (lane == 0) {
+    red[2][wave] = sp;
+    red[3][wave] = sq;
+    red[4][wave] = a;
+  }
+  __syncthreads();
+  if (t == 0) {
+    PairChunk pc;
+    pc.mt = rt;
+    pc.md = rd;
+    pc.sp = pc.sq = pc.a = 0.0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      pc.sp += double(red[2][w]);
+      pc.sq += double(red[3][w]);
+      pc.a += double(red[4][w]);
+    }
+    *out = pc;
+  }
+}
+
+// bf16 rows with 16-byte alignment: the hot kernel.
+__global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__restrict__ target,
+                                                             const void *__restrict__ draft, int64_t V, int32_t nc,
+                                                             const WorkItem *__restrict__ work,
+                                                             const int32_t *__restrict__ draft_tokens,
+                                                             PairChunk *__restrict__ out,
+                                                             Gathered *__restrict__ gathered) {
+  __shared__ float red[5][kWaves];
+  const int64_t unit = blockIdx.x;
+  const int64_t k = unit / nc;
+  const int64_t chunk = unit - k * nc;
+  const WorkItem w = work[k];
+  if (w.target_row < 0) return;
+  const int t = threadIdx.x;
+  const float c = __uint_as_float(w.scale_bits);
+  const char *trow = (const char *)target + size_t(w.target_row) * size_t(V) * 2;
+  const char *drow = (const char *)draft + size_t(w.pair) * size_t(V) * 2;
+  const RawBf16 rt_ = load_raw_bf16(trow, V, chunk, t);
+  const RawBf16 rd_ = load_raw_bf16(drow, V, chunk, t);
+
+  // chunk maxima -> the reference shifts every exponential of the chunk uses
+  const float Mt = block_max(raw_max(rt_), red[0]);
+  const float Md = block_max(raw_max(rd_), red[1]);
+  const float rt = Mt * c, rd = Md * c;
+  float s[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  acc_vec(rt_.v0, rd_.v0, c, rt, rd, s);
+  acc_vec(rt_.v1, rd_.v1, c, rt, rd, s);
+  acc_vec(rt_.v2, rd_.v2, c, rt, rd, s);
+  acc_vec(rt_.v3, rd_.v3, c, rt, rd, s);
+
+  // the logits at the drafted token, from registers
+  // a token outside [0, V) never matches (its sequence is flagged later)
+  const int64_t local = int64_t(draft_tokens[w.pair]) - chunk * kChunk;
+  if (local >= 0 && local < kChunk) {
+    int ot, oi;
+    Layout<DSDE_BF16, true>::owner(local, &ot, &oi);
+    if (t == ot) {
+      // select with compile-time slots only: a runtime index into the
+      // register arrays would put them in scratch memory
+      float a = 0.f, b = 0.f;
+#pragma unroll
+      for (int i = 0; i < kEltsPerThread; ++i)
+        if (i == oi) {
+          a = pick_bf16(rt_, i);
+          b = pick_bf16(rd_, i);
+        }
+      gathered[w.pair] = Gathered{a, b};
+    }
+  }
+  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.pair) * nc + chunk);
+}
+
+// fp32 rows, or rows without 16-byte alignment.
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__restrict__ target,
+                                                                const void *__restrict__ draft, int64_t V,
+                                                                int32_t nc, const WorkItem *__restrict__ work,
+                                                                const int32_t *__restrict__ draft_tokens,
+                                                                PairChunk *__restrict__ out,
+                                                                Gathered *__restrict__ gathered) {
+  __shared__ float red[5][kWaves];
+  const int64_t unit = blockIdx.x;
+  const int64_t k = unit / nc;
+  const int64_t chunk = unit - k * nc;
+  const WorkItem w = work[k];
+  if (w.target_row < 0) return;
+  const int t = threadIdx.x;
+  const float c = __uint_as_float(w.scale_bits);
+  const size_t esz = DT == DSDE_BF16 ? 2 : 4;
+  const char *trow = (const char *)target + size_t(w.target_row) * size_t(V) * esz;
+  const char *drow = (const char *)draft + size_t(w.pair) * size_t(V) * esz;
+  float zt[kEltsPerThread], zd[kEltsPerThread];
+  load_chunk_f32<DT, VEC>(trow, V, chunk, t, zt);
+  load_chunk_f32<DT, VEC>(drow, V, chunk, t, zd);
+  float mt = zt[0], md = zd[0];
+#pragma unroll
+  for (int i = 1; i < kEltsPerThread; ++i) {
+    mt = fmaxf(mt, zt[i]);
+    md = fmaxf(md, zd[i]);
+  }
+  const float Mt = block_max(mt, red[0]);
+  const float Md = block_max(md, red[1]);
+  const float rt = Mt * c, rd = Md * c;
+  float s[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < kEltsPerThread; i += 2) {
+    acc_pair(zt[i], zd[i], c, rt, rd, s[0], s[1], s[2]);
+    acc_pair(zt[i + 1], zd[i + 1], c, rt, rd, s[3], s[4], s[5]);
+  }
+  // a token outside [0, V) never matches (its sequence is flagged later)
+  const int64_t local = int64_t(draft_tokens[w.pair]) - chunk * kChunk;
+  if (local >= 0 && local < kChunk) {
+    int ot, oi;
+    Layout<DT, VEC>::owner(local, &ot, &oi);
+    if (t == ot) {
+      float a = 0.f, b = 0.f;
+#pragma unroll
+      for (int i = 0; i < kEltsPerThread; ++i)
+        if (i == oi) {
+          a = zt[i];
+          b = zd[i];
+        }
+      gathered[w.pair] = Gathered{a, b};
+    }
+  }
+  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.pair) * nc + chunk);
+}
+
+}  // namespace
+
+static inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// With profiling events set, `stop` is attached to the completion of the
+// statistics dispatch and `start` to the completion of the set-up dispatch
+// just before it, so that the interval is the statistics kernel alone (a
+// start event attached to a dispatch is stamped when the packet is
+// processed, which can be while the previous kernel still runs).
+template <typename K, typename... Args>
+static void launch_timed(K kernel, dim3 grid, dim3 block, hipStream_t stream, hipEvent_t done, Args... args) {
+  if (done)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, nullptr, done, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, stream, args...);
+}
+
+bool rows_vectorizable(const VerifyArgs &a) {
+  return aligned16(a.target) && (a.N == 0 || aligned16(a.draft)) &&
+         (a.dtype == DSDE_BF16 ? a.V % 8 == 0 : a.V % 4 == 0);
+}
+
+void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gathered *gath) {
+  const int32_t nc = int32_t(num_chunks(a.V));
+  const bool prof = a.prof_start && a.prof_stop && a.N > 0;
+  launch_timed(setup_kernel, dim3(1), dim3(1024), a.stream, prof ? a.prof_start : nullptr, a.B, a.N, a.k_max,
+               a.sl, a.cu_sl, a.temperature, a.seq_err, work);
+  if (a.N == 0) return;
+  const bool vec = rows_vectorizable(a);
+  const dim3 grid(unsigned(a.N * nc)), block(kThreads);
+  hipEvent_t done = prof ? a.prof_stop : nullptr;
+  const void *T = a.target, *D = a.draft;
+  const int64_t V = a.V;
+  const int32_t *tokens = a.draft_tokens;
+  const WorkItem *w = work;
+  if (a.dtype == DSDE_BF16 && vec)
+    launch_timed(stats_kernel_bf16, grid, block, a.stream, done, T, D, V, nc, w, tokens, part, gath);
+  else if (a.dtype == DSDE_BF16)
+    launch_timed(stats_kernel_generic<DSDE_BF16, false>, grid, block, a.stream, done, T, D, V, nc, w, tokens, part,
+                 gath);
+  else if (vec)
+    launch_timed(stats_kernel_generic<DSDE_FP32, true>, grid, block, a.stream, done, T, D, V, nc, w, tokens, part,
+                 gath);
+  else
+    launch_timed(stats_kernel_generic<DSDE_FP32, false>, grid, block, a.stream, done, T, D, V, nc, w, tokens, part,
+                 gath);
+}
+
+}  // namespace dsde

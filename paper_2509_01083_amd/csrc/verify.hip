@@ -1,426 +1,29 @@
 // Batched speculative verification with ragged per-sequence speculation
-// lengths on gfx950: row statistics + per-token KLD, acceptance scan, and the
-// inverse-CDF draw from the residual max(0, p - q) or the bonus row
-// (speculative sampling, Sec. 2.1; ragged layout, bonus and pad, Sec. 3.2;
-// per-token KLD of the SL adapter, Sec. 3.1.2).
+// lengths on gfx950 (speculative sampling, Sec. 2.1; ragged layout, bonus and
+// pad, Sec. 3.2; per-token KLD of the SL adapter, Sec. 3.1.2).
 //
 // Kernels, in launch order on the caller's stream:
-//   setup_kernel       one workgroup: validates the packed layout and writes
-//                      the work list of the statistics pass (target row and
-//                      scale of every drafted pair, in sequence order).
-//   stats_kernel       one workgroup per (row pair, 8192-logit chunk): reads
-//                      the chunk of the target and draft rows once and writes
-//                      max-shifted exponential sums of p and q and the KL
-//                      accumulator; also captures the two logits at the drafted
-//                      token.  Carries almost all HBM bytes of the step.
-//   accept_kernel      one workgroup per sequence: per-sequence input checks,
-//                      the chunk partials of every drafted pair combined by
-//                      groups of lanes (fp64), the KLD, u < p(x)/q(x) for every
-//                      drafted position (fp64) and the first rejection; writes
-//                      the draw job.  Fused: the signal update of the sequence.
-//   draw_chunk_kernel  one workgroup per (sequence, chunk): the chunk's total of
-//                      the draw weights, max(0, p - q) of the rejected pair or
-//                      the bonus row's exponentials.
-//   finish_kernel      one workgroup per sequence: prefix over the chunk totals
-//                      (fp64), then an ordered scan inside the one chunk that
-//                      holds u' * Z.  Fused: one extra workgroup computes the
-//                      batch cap and the next speculation lengths.
+//   setup_kernel, stats_kernel   (stats.hip) layout check, work list, and the
+//                      row statistics of every drafted pair, chunk by chunk.
+//   seq_kernel         one workgroup per sequence: combines the chunk partials
+//                      of its drafted pairs (fp64), KLD, acceptance u < p(x)/q(x)
+//                      (fp64) up to the first rejection, then the draw: the
+//                      residual max(0, p - q) of the rejected pair (or the bonus
+//                      row) streamed one wavefront per chunk with the chunk
+//                      totals in LDS, a fixed-order fp64 prefix to the chunk
+//                      holding u' * Z, and a block-wide ordered scan inside it.
+//                      Fused step: one wavefront also runs the signal update.
+//   next_sl_kernel     (signal.hip, fused step only) batch cap and next lengths.
 //
 // Every reduction runs in a fixed order, so results are bitwise reproducible.
-#include <hip/hip_ext.h>
 #include <math.h>
 
 #include "common.hpp"
+#include "row_io.hpp"
 #include "signal_device.hpp"
 
 namespace dsde {
 namespace {
-
-// bf16 -2^96: padding for logits past V.  It is below every admissible logit
-// (|z| <= 2^64), its exponential is exactly 0, and differences of two padding
-// values stay finite, so padding adds exactly nothing to any sum.
-constexpr uint32_t kPadBf16x2 = 0xef80ef80u;
-constexpr float kPadF32 = -7.9228162514264337593543950336e28f;  // -2^96
-
-__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// 2^x on the transcendental unit (about 1 ulp; results below 2^-126 flush to 0).
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
-__device__ __forceinline__ float load_logit(const void *base, int dtype, int64_t idx) {
-  if (dtype == DSDE_BF16) return __uint_as_float(uint32_t(((const uint16_t *)base)[idx]) << 16);
-  return ((const float *)base)[idx];
-}
-
-// Block-wide max of one value per thread (all threads receive it).
-__device__ __forceinline__ float block_max(float v, float *lds) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  v = wave_max(v);
-  if (lane == 0) lds[wave] = v;
-  __syncthreads();
-  float m = lds[0];
-#pragma unroll
-  for (int w = 1; w < kWaves; ++w) m = fmaxf(m, lds[w]);
-  __syncthreads();
-  return m;
-}
-
-// ---------------------------------------------------------------------------
-// chunk of a row held by one workgroup
-// ---------------------------------------------------------------------------
-//
-// The 8192 logits of chunk k of a row are spread over the 256 threads so that
-// each wavefront load is contiguous.  Thread t owns slots i = 0..31:
-//   bf16, 16-byte rows : logit 8 * (1024 k + 256 (i / 8) + t) + i % 8  (4 x uint4)
-//   fp32, 16-byte rows : logit 4 * (2048 k + 256 (i / 4) + t) + i % 4  (8 x float4)
-//   any other row      : logit 8192 k + 256 i + t                       (32 scalars)
-// Every load uses an in-bounds (clamped) index and the value is replaced by
-// padding past V, so the loads never branch.
-
-template <int DT, bool VEC>
-struct Layout;
-template <>
-struct Layout<DSDE_BF16, true> {
-  __device__ static int64_t index(int64_t chunk, int i, int t) {
-    return 8 * (chunk * 1024 + (i / 8) * 256 + t) + (i % 8);
-  }
-  __device__ static void owner(int64_t local, int *t, int *i) {
-    *t = int((local >> 3) & 255);
-    *i = int((local >> 11) * 8 + (local & 7));
-  }
-};
-template <>
-struct Layout<DSDE_FP32, true> {
-  __device__ static int64_t index(int64_t chunk, int i, int t) {
-    return 4 * (chunk * 2048 + (i / 4) * 256 + t) + (i % 4);
-  }
-  __device__ static void owner(int64_t local, int *t, int *i) {
-    *t = int((local >> 2) & 255);
-    *i = int((local >> 10) * 4 + (local & 3));
-  }
-};
-template <int DT>
-struct Layout<DT, false> {
-  __device__ static int64_t index(int64_t chunk, int i, int t) { return chunk * kChunk + int64_t(i) * 256 + t; }
-  __device__ static void owner(int64_t local, int *t, int *i) {
-    *t = int(local & 255);
-    *i = int(local >> 8);
-  }
-};
-
-// Raw bf16 chunk of one row: 4 x uint4 per thread.
-struct RawBf16 {
-  uint4 v0, v1, v2, v3;
-};
-
-__device__ __forceinline__ RawBf16 load_raw_bf16(const void *row, int64_t V, int64_t chunk, int t) {
-  const uint4 *p = (const uint4 *)row;
-  const int64_t last = V / 8 - 1;
-  const int64_t i0 = chunk * 1024 + t;
-  const uint4 pad = make_uint4(kPadBf16x2, kPadBf16x2, kPadBf16x2, kPadBf16x2);
-  const uint4 a0 = p[min(i0, last)], a1 = p[min(i0 + 256, last)];
-  const uint4 a2 = p[min(i0 + 512, last)], a3 = p[min(i0 + 768, last)];
-  RawBf16 r;
-  r.v0 = i0 <= last ? a0 : pad;
-  r.v1 = i0 + 256 <= last ? a1 : pad;
-  r.v2 = i0 + 512 <= last ? a2 : pad;
-  r.v3 = i0 + 768 <= last ? a3 : pad;
-  return r;
-}
-
-__device__ __forceinline__ float max2(uint32_t w) { return fmaxf(bf_lo(w), bf_hi(w)); }
-__device__ __forceinline__ float vmax(uint4 v) {
-  return fmaxf(fmaxf(max2(v.x), max2(v.y)), fmaxf(max2(v.z), max2(v.w)));
-}
-__device__ __forceinline__ float raw_max(const RawBf16 &r) {
-  return fmaxf(fmaxf(vmax(r.v0), vmax(r.v1)), fmaxf(vmax(r.v2), vmax(r.v3)));
-}
-__device__ __forceinline__ float pick_bf16(const RawBf16 &r, int i) {
-  const uint4 v = (i >> 3) == 0 ? r.v0 : (i >> 3) == 1 ? r.v1 : (i >> 3) == 2 ? r.v2 : r.v3;
-  const int w = (i >> 1) & 3;
-  const uint32_t x = w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
-  return (i & 1) ? bf_hi(x) : bf_lo(x);
-}
-
-// Statistics of one logit pair with references rt, rd (log2 domain).
-__device__ __forceinline__ void acc_pair(float zt, float zd, float c, float rt, float rd, float &sp, float &sq,
-                                         float &a) {
-  const float at = fmaf(zt, c, -rt), ad = fmaf(zd, c, -rd);
-  const float et = fast_exp2(at), ed = fast_exp2(ad);
-  sp += et;
-  sq += ed;
-  a = fmaf(et, at - ad, a);
-}
-__device__ __forceinline__ void acc_word(uint32_t t, uint32_t d, float c, float rt, float rd, float (&s)[6]) {
-  acc_pair(bf_lo(t), bf_lo(d), c, rt, rd, s[0], s[1], s[2]);
-  acc_pair(bf_hi(t), bf_hi(d), c, rt, rd, s[3], s[4], s[5]);
-}
-__device__ __forceinline__ void acc_vec(uint4 t, uint4 d, float c, float rt, float rd, float (&s)[6]) {
-  acc_word(t.x, d.x, c, rt, rd, s);
-  acc_word(t.y, d.y, c, rt, rd, s);
-  acc_word(t.z, d.z, c, rt, rd, s);
-  acc_word(t.w, d.w, c, rt, rd, s);
-}
-
-// Generic chunk of one row as 32 floats (fp32 rows, or rows without 16-byte alignment).
-template <int DT, bool VEC>
-__device__ __forceinline__ void load_chunk_f32(const void *row, int64_t V, int64_t chunk, int t,
-                                               float (&z)[kEltsPerThread]) {
-  if constexpr (VEC && DT == DSDE_FP32) {
-    const float4 *p = (const float4 *)row;
-    const int64_t last = V / 4 - 1;
-#pragma unroll
-    for (int g = 0; g < 8; ++g) {
-      const int64_t i = chunk * 2048 + g * 256 + t;
-      const float4 w = p[min(i, last)];
-      const bool ok = i <= last;
-      z[g * 4 + 0] = ok ? w.x : kPadF32;
-      z[g * 4 + 1] = ok ? w.y : kPadF32;
-      z[g * 4 + 2] = ok ? w.z : kPadF32;
-      z[g * 4 + 3] = ok ? w.w : kPadF32;
-    }
-  } else if constexpr (VEC && DT == DSDE_BF16) {
-    const RawBf16 r = load_raw_bf16(row, V, chunk, t);
-#pragma unroll
-    for (int i = 0; i < kEltsPerThread; ++i) z[i] = pick_bf16(r, i);
-  } else {
-#pragma unroll
-    for (int i = 0; i < kEltsPerThread; ++i) {
-      const int64_t v = chunk * kChunk + int64_t(i) * 256 + t;
-      const float x = load_logit(row, DT, v < V ? v : V - 1);
-      z[i] = v < V ? x : kPadF32;
-    }
-  }
-}
-
-// R consecutive logits of a row, from `start` (a multiple of R, R a multiple
-// of 8), padded past V.
-template <int DT, bool VEC, int R>
-__device__ __forceinline__ void load_run(const void *row, int64_t V, int64_t start, float (&z)[R]) {
-  if constexpr (VEC && DT == DSDE_BF16) {
-    const uint4 *p = (const uint4 *)row;
-    const int64_t last = V / 8 - 1;
-#pragma unroll
-    for (int q = 0; q < R / 8; ++q) {
-      const int64_t i = start / 8 + q;
-      const uint4 a = p[min(i, last)];
-      const uint4 v = i <= last ? a : make_uint4(kPadBf16x2, kPadBf16x2, kPadBf16x2, kPadBf16x2);
-      z[8 * q + 0] = bf_lo(v.x);
-      z[8 * q + 1] = bf_hi(v.x);
-      z[8 * q + 2] = bf_lo(v.y);
-      z[8 * q + 3] = bf_hi(v.y);
-      z[8 * q + 4] = bf_lo(v.z);
-      z[8 * q + 5] = bf_hi(v.z);
-      z[8 * q + 6] = bf_lo(v.w);
-      z[8 * q + 7] = bf_hi(v.w);
-    }
-  } else if constexpr (VEC && DT == DSDE_FP32) {
-    const float4 *p = (const float4 *)row;
-    const int64_t last = V / 4 - 1;
-#pragma unroll
-    for (int q = 0; q < R / 4; ++q) {
-      const int64_t i = start / 4 + q;
-      const float4 a = p[min(i, last)];
-      const bool ok = i <= last;
-      z[4 * q + 0] = ok ? a.x : kPadF32;
-      z[4 * q + 1] = ok ? a.y : kPadF32;
-      z[4 * q + 2] = ok ? a.z : kPadF32;
-      z[4 * q + 3] = ok ? a.w : kPadF32;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < R; ++i) {
-      const int64_t v = start + i;
-      const float x = load_logit(row, DT, v < V ? v : V - 1);
-      z[i] = v < V ? x : kPadF32;
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// set-up
-// ---------------------------------------------------------------------------
-
-__global__ __launch_bounds__(1024) void setup_kernel(int32_t B, int64_t N, int32_t k_max,
-                                                     const int32_t *__restrict__ sl,
-                                                     const int32_t *__restrict__ cu_sl,
-                                                     const float *__restrict__ temperature,
-                                                     uint32_t *__restrict__ seq_err, WorkItem *__restrict__ work) {
-  const int t = threadIdx.x;
-  const int64_t c_first = cu_sl[0], c_last = cu_sl[B];
-  int bad = 0;
-  for (int32_t b = t; b < B; b += blockDim.x) {
-    const int64_t s = sl[b];
-    if (s < 0 || s > k_max || int64_t(cu_sl[b + 1]) - int64_t(cu_sl[b]) != s) bad = 1;
-  }
-  bad = __syncthreads_or(bad);
-  if (c_first != 0 || c_last != N) bad = 1;
-  if (bad) {
-    for (int32_t b = t; b < B; b += blockDim.x) seq_err[b] = DSDE_ERR_LAYOUT;
-    for (int64_t k = t; k < N; k += blockDim.x) work[k] = WorkItem{int32_t(k), -1, 0u, 0};
-    return;
-  }
-  for (int32_t b = t; b < B; b += blockDim.x) {
-    const int32_t first = cu_sl[b], s = sl[b];
-    seq_err[b] = 0u;
-    // the same expression as every later kernel's scale; a temperature outside
-    // the admissible range is flagged by the acceptance kernel
-    const uint32_t cbits = __float_as_uint(kLog2e / temperature[b]);
-    for (int32_t j = 0; j < s; ++j) work[first + j] = WorkItem{first + j, first + b + j, cbits, 0};
-  }
-}
-
-// ---------------------------------------------------------------------------
-// row statistics of every drafted pair
-// ---------------------------------------------------------------------------
-
-// Chunk sums of one workgroup -> one PairChunk (fixed order: lanes, then waves in fp64).
-__device__ __forceinline__ void write_pair_chunk(float rt, float rd, float sp, float sq, float a, float (*red)[kWaves],
-                                                 PairChunk *out) {
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  sp = wave_sum(sp);
-  sq = wave_sum(sq);
-  a = wave_sum(a);
-  if (lane == 0) {
-    red[2][wave] = sp;
-    red[3][wave] = sq;
-    red[4][wave] = a;
-  }
-  __syncthreads();
-  if (t == 0) {
-    PairChunk pc;
-    pc.mt = rt;
-    pc.md = rd;
-    pc.sp = pc.sq = pc.a = 0.0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      pc.sp += double(red[2][w]);
-      pc.sq += double(red[3][w]);
-      pc.a += double(red[4][w]);
-    }
-    *out = pc;
-  }
-}
-
-// bf16 rows with 16-byte alignment: the hot kernel.
-__global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__restrict__ target,
-                                                             const void *__restrict__ draft, int64_t V, int32_t nc,
-                                                             const WorkItem *__restrict__ work,
-                                                             const int32_t *__restrict__ draft_tokens,
-                                                             PairChunk *__restrict__ out,
-                                                             Gathered *__restrict__ gathered) {
-  __shared__ float red[5][kWaves];
-  const int64_t unit = blockIdx.x;
-  const int64_t k = unit / nc;
-  const int64_t chunk = unit - k * nc;
-  const WorkItem w = work[k];
-  if (w.target_row < 0) return;
-  const int t = threadIdx.x;
-  const float c = __uint_as_float(w.scale_bits);
-  const char *trow = (const char *)target + size_t(w.target_row) * size_t(V) * 2;
-  const char *drow = (const char *)draft + size_t(w.pair) * size_t(V) * 2;
-  const RawBf16 rt_ = load_raw_bf16(trow, V, chunk, t);
-  const RawBf16 rd_ = load_raw_bf16(drow, V, chunk, t);
-
-  // chunk maxima -> the reference shifts every exponential of the chunk uses
-  const float Mt = block_max(raw_max(rt_), red[0]);
-  const float Md = block_max(raw_max(rd_), red[1]);
-  const float rt = Mt * c, rd = Md * c;
-  float s[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  acc_vec(rt_.v0, rd_.v0, c, rt, rd, s);
-  acc_vec(rt_.v1, rd_.v1, c, rt, rd, s);
-  acc_vec(rt_.v2, rd_.v2, c, rt, rd, s);
-  acc_vec(rt_.v3, rd_.v3, c, rt, rd, s);
-
-  // the logits at the drafted token, from registers
-  // a token outside [0, V) never matches (its sequence is flagged later)
-  const int64_t local = int64_t(draft_tokens[w.pair]) - chunk * kChunk;
-  if (local >= 0 && local < kChunk) {
-    int ot, oi;
-    Layout<DSDE_BF16, true>::owner(local, &ot, &oi);
-    if (t == ot) {
-      // select with compile-time slots only: a runtime index into the
-      // register arrays would put them in scratch memory
-      float a = 0.f, b = 0.f;
-#pragma unroll
-      for (int i = 0; i < kEltsPerThread; ++i)
-        if (i == oi) {
-          a = pick_bf16(rt_, i);
-          b = pick_bf16(rd_, i);
-        }
-      gathered[w.pair] = Gathered{a, b};
-    }
-  }
-  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.pair) * nc + chunk);
-}
-
-// fp32 rows, or rows without 16-byte alignment.
-template <int DT, bool VEC>
-__global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__restrict__ target,
-                                                                const void *__restrict__ draft, int64_t V,
-                                                                int32_t nc, const WorkItem *__restrict__ work,
-                                                                const int32_t *__restrict__ draft_tokens,
-                                                                PairChunk *__restrict__ out,
-                                                                Gathered *__restrict__ gathered) {
-  __shared__ float red[5][kWaves];
-  const int64_t unit = blockIdx.x;
-  const int64_t k = unit / nc;
-  const int64_t chunk = unit - k * nc;
-  const WorkItem w = work[k];
-  if (w.target_row < 0) return;
-  const int t = threadIdx.x;
-  const float c = __uint_as_float(w.scale_bits);
-  const size_t esz = DT == DSDE_BF16 ? 2 : 4;
-  const char *trow = (const char *)target + size_t(w.target_row) * size_t(V) * esz;
-  const char *drow = (const char *)draft + size_t(w.pair) * size_t(V) * esz;
-  float zt[kEltsPerThread], zd[kEltsPerThread];
-  load_chunk_f32<DT, VEC>(trow, V, chunk, t, zt);
-  load_chunk_f32<DT, VEC>(drow, V, chunk, t, zd);
-  float mt = zt[0], md = zd[0];
-#pragma unroll
-  for (int i = 1; i < kEltsPerThread; ++i) {
-    mt = fmaxf(mt, zt[i]);
-    md = fmaxf(md, zd[i]);
-  }
-  const float Mt = block_max(mt, red[0]);
-  const float Md = block_max(md, red[1]);
-  const float rt = Mt * c, rd = Md * c;
-  float s[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int i = 0; i < kEltsPerThread; i += 2) {
-    acc_pair(zt[i], zd[i], c, rt, rd, s[0], s[1], s[2]);
-    acc_pair(zt[i + 1], zd[i + 1], c, rt, rd, s[3], s[4], s[5]);
-  }
-  // a token outside [0, V) never matches (its sequence is flagged later)
-  const int64_t local = int64_t(draft_tokens[w.pair]) - chunk * kChunk;
-  if (local >= 0 && local < kChunk) {
-    int ot, oi;
-    Layout<DT, VEC>::owner(local, &ot, &oi);
-    if (t == ot) {
-      float a = 0.f, b = 0.f;
-#pragma unroll
-      for (int i = 0; i < kEltsPerThread; ++i)
-        if (i == oi) {
-          a = zt[i];
-          b = zd[i];
-        }
-      gathered[w.pair] = Gathered{a, b};
-    }
-  }
-  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.pair) * nc + chunk);
-}
 
 // ---------------------------------------------------------------------------
 // per-sequence kernel: acceptance, draw weights and draw
@@ -1012,24 +615,12 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
 
 }  // namespace
 
-static inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-
 template <int DT, bool VEC>
 static void launch_seq(const VerifyArgs &a, const StepParams &P, const SignalArgs &S) {
   if (a.signal)
     seq_kernel<DT, VEC, true><<<dim3(unsigned(a.B)), dim3(kSeqThreads), 0, a.stream>>>(P, S);
   else
     seq_kernel<DT, VEC, false><<<dim3(unsigned(a.B)), dim3(kSeqThreads), 0, a.stream>>>(P, S);
-}
-
-// The statistics pass; with profiling events set, the events are attached to
-// the dispatch itself (they time exactly this kernel).
-template <typename K, typename... Args>
-static void launch_stats(K kernel, dim3 grid, const VerifyArgs &a, Args... args) {
-  if (a.prof_start && a.prof_stop)
-    hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, a.stream, a.prof_start, a.prof_stop, 0, args...);
-  else
-    hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, a.stream, args...);
 }
 
 int launch_verify(const VerifyArgs &a) {
@@ -1040,27 +631,8 @@ int launch_verify(const VerifyArgs &a) {
   PairChunk *part = (PairChunk *)(ws + L.pair_chunk);
   Gathered *gath = (Gathered *)(ws + L.gathered);
   (void)hipGetLastError();
-  setup_kernel<<<dim3(1), dim3(1024), 0, a.stream>>>(a.B, a.N, a.k_max, a.sl, a.cu_sl, a.temperature, a.seq_err,
-                                                    work);
-  const bool vec = aligned16(a.target) && (a.N == 0 || aligned16(a.draft)) &&
-                   (a.dtype == DSDE_BF16 ? a.V % 8 == 0 : a.V % 4 == 0);
-  if (a.N > 0) {
-    const dim3 grid(unsigned(a.N * nc));
-    const void *T = a.target, *D = a.draft;
-    const int64_t V = a.V;
-    const int32_t *tokens = a.draft_tokens;
-    if (a.dtype == DSDE_BF16 && vec)
-      launch_stats(stats_kernel_bf16, grid, a, T, D, V, nc, (const WorkItem *)work, tokens, part, gath);
-    else if (a.dtype == DSDE_BF16)
-      launch_stats(stats_kernel_generic<DSDE_BF16, false>, grid, a, T, D, V, nc, (const WorkItem *)work, tokens,
-                   part, gath);
-    else if (vec)
-      launch_stats(stats_kernel_generic<DSDE_FP32, true>, grid, a, T, D, V, nc, (const WorkItem *)work, tokens,
-                   part, gath);
-    else
-      launch_stats(stats_kernel_generic<DSDE_FP32, false>, grid, a, T, D, V, nc, (const WorkItem *)work, tokens,
-                   part, gath);
-  }
+  launch_stats_pass(a, work, part, gath);
+  const bool vec = rows_vectorizable(a);
   StepParams P;
   P.target = a.target;
   P.draft = a.draft;
