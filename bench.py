@@ -36,6 +36,7 @@ def parse():
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU time of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-stream-ceiling", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM traffic of the row-statistics kernel (from rocprofv3 counters)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -143,6 +144,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "B": B, "N": N, "V": V, "rows_per_step": rows, "k_max": k_max,
                    "logit_bytes_per_step": rows * V * esz, "seed": args.seed},
+        "positions_per_s": N / (ms_per_step * 1e-3),
         "hbm_gbps_algorithmic": alg_bytes / (ms_per_step * 1e-3) / 1e9,
         "hbm_frac_algorithmic": alg_bytes / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBPS,
         "wall_ms_per_step": wall * 1e3 / args.steps,
@@ -153,6 +155,28 @@ def main():
                      "kernel_ms": k1_ms, "algorithmic_bytes": k1_bytes},
         "cpu_baseline": None,
     }
+
+    # streaming-read ceiling of this GPU: the library's read-reduce probe over
+    # 4 GiB (16x the last-level cache), timed with the same fence-free events
+    if not args.no_stream_ceiling:
+        buf = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
+        acc = torch.empty((4 << 30) // 32768, dtype=torch.int32, device=dev)
+        for _ in range(2):
+            dsde.stream_read(buf, acc)
+        e0, e1 = HipEvent(), HipEvent()
+        reps = 10
+        torch.cuda.synchronize()
+        _record(e0, stream)
+        for _ in range(reps):
+            dsde.stream_read(buf, acc)
+        _record(e1, stream)
+        torch.cuda.synchronize()
+        ceil_gbps = reps * buf.numel() / (e0.elapsed_ms(e1) * 1e-3) / 1e9
+        e0.destroy()
+        e1.destroy()
+        del buf
+        result["stream_read_ceiling"] = {"gbps": ceil_gbps, "bytes": 4 << 30, "launches": reps}
+        result["roofline"]["frac_of_stream_ceiling"] = k1_gbps / ceil_gbps
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"], result["parity"] = cpu_baseline(copies[last], outs[last], st, args.cpu_seconds)
@@ -168,6 +192,14 @@ def main():
         result["copy_calibration"] = {"kernel": "bitwise_not", "read_bytes": 4 * n, "write_bytes": 4 * n,
                                       "launches": 3}
     print(json.dumps(result), flush=True)
+
+
+def _record(ev, stream):
+    """hipEventRecord of a HipEvent on a torch stream."""
+    import ctypes
+    HipEvent._hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    if HipEvent._hip.hipEventRecord(ev.handle, ctypes.c_void_p(stream.cuda_stream)) != 0:
+        raise RuntimeError("hipEventRecord failed")
 
 
 class HipEvent:

@@ -199,6 +199,20 @@ int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t d
                   void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * Measurement utility, not part of the method: reads `bytes` bytes of device
+ * memory at `buf` with the statistics pass's access pattern (one workgroup per
+ * 32 KiB, 16-byte vector loads, 1 KiB contiguous per wavefront load) and
+ * writes the XOR of every 32-bit word of 32 KiB unit u to out[u].  Timed over
+ * a buffer much larger than the last-level cache it gives the streaming-read
+ * ceiling the row statistics kernel is compared against.
+ *   buf      device pointer, 16-byte aligned
+ *   bytes    a positive multiple of 16
+ *   out      device array of ceil(bytes / 32768) uint32
+ * Returns DSDE_INVALID_ARG for a NULL or misaligned pointer or a bad size.
+ */
+int32_t dsde_stream_read(const void *buf, int64_t bytes, uint32_t *out, void *stream);
+
+/*
  * Profiling hook: when both events are non-NULL (hipEvent_t, created with
  * timing enabled), every later dsde_verify or dsde_step with N > 0 attaches
  * `start` to the completion of its set-up kernel and `stop` to the completion

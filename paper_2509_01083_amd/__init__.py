@@ -19,7 +19,7 @@ FP32, BF16 = 0, 1
 ERR_LAYOUT, ERR_TOKEN, ERR_LOGIT, ERR_TEMP, ERR_UNIFORM, ERR_SIGNAL, ERR_STATE = 1, 2, 4, 8, 16, 32, 64
 MAX_K = 63
 EXPORTS = ("dsde_abi_version", "dsde_status_string", "dsde_verify_workspace_bytes", "dsde_verify",
-           "dsde_step", "dsde_kld_signal", "dsde_next_sl", "dsde_set_profile_events")
+           "dsde_step", "dsde_kld_signal", "dsde_next_sl", "dsde_set_profile_events", "dsde_stream_read")
 
 _lib = None
 
@@ -56,6 +56,8 @@ def load(path: str = LIB_PATH):
     lib.dsde_next_sl.argtypes = [i32, P, P, P, f32, i32, P, P, P, P, P]
     lib.dsde_set_profile_events.restype = i32
     lib.dsde_set_profile_events.argtypes = [P, P]
+    lib.dsde_stream_read.restype = i32
+    lib.dsde_stream_read.argtypes = [P, i64, P, P]
     _lib = lib
     return lib
 
@@ -241,3 +243,16 @@ def set_profile_events(start=None, stop=None):
             return None
         return ctypes.c_void_p(ev if isinstance(ev, int) else ev.cuda_event)
     _check(lib.dsde_set_profile_events(handle(start), handle(stop)))
+
+
+def stream_read(buf, out):
+    """Streaming-read ceiling probe: reads every byte of the contiguous device
+    tensor ``buf`` (one workgroup per 32 KiB) and writes each unit's XOR to
+    ``out`` (int32, at least ceil(bytes / 32768) elements) on the current stream."""
+    import torch
+    lib = load()
+    nbytes = buf.numel() * buf.element_size()
+    if out.numel() < (nbytes + 32767) // 32768:
+        raise DsdeError("stream_read: out holds fewer than one word per 32 KiB")
+    _check(lib.dsde_stream_read(ctypes.c_void_p(buf.data_ptr()), nbytes, ctypes.c_void_p(out.data_ptr()),
+                                ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)))

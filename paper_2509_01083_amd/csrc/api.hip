@@ -184,4 +184,10 @@ int32_t dsde_set_profile_events(void *start, void *stop) {
   return DSDE_OK;
 }
 
+int32_t dsde_stream_read(const void *buf, int64_t bytes, uint32_t *out, void *stream) {
+  if (!buf || !out || bytes <= 0 || bytes % 16 != 0) return DSDE_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(buf) & 15u) != 0) return DSDE_INVALID_ARG;
+  return dsde::launch_stream_read(buf, bytes, out, static_cast<hipStream_t>(stream));
+}
+
 }  // extern "C"

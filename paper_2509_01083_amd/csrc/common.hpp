@@ -115,6 +115,7 @@ int launch_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu
                       float *hist, int32_t *head, int32_t *count, int32_t W, int32_t n_short, int32_t n_long,
                       float delta, float eps, float *mu_last, float *var_short, float *var_long, float *wvir,
                       float *sf, uint32_t *seq_err, hipStream_t stream);
+int launch_stream_read(const void *buf, int64_t bytes, uint32_t *out, hipStream_t stream);
 int launch_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max, float sl_min,
                    int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err, bool or_err,
                    hipStream_t stream);

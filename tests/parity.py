@@ -31,8 +31,52 @@ def run_verify(dsde, step, row_lse=True):
     return res
 
 
-def compare_verify(got, ref, sl, cu_sl, label=""):
-    """Asserts the comparison rules; returns a small report."""
+def _decode(row):
+    row = np.asarray(row)
+    if row.dtype == np.uint16:
+        return (row.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return row.astype(np.float64)
+
+
+def _softmax(z, T):
+    s = z / float(T)
+    s = s - s.max()
+    e = np.exp(s)
+    return e / e.sum()
+
+
+def emission_is_valid(got, host, b, pad_id=-1):
+    """A tie sequence's outputs are one of the emissions the method allows: the
+    accepted drafts are a prefix of the drafted tokens, and the drawn token has
+    positive weight (up to fp32 rounding) in the draw the accepted count implies
+    (residual of the first rejected pair, or p of the bonus row), then padding."""
+    sl, cu = host["sl"], host["cu_sl"]
+    s, first, V = int(sl[b]), int(cu[b]), int(host["V"])
+    a = int(got["accepted"][b])
+    toks = got["tokens"][b]
+    if not 0 <= a <= s:
+        return False
+    if not np.array_equal(toks[:a], host["draft_tokens"][first:first + a]):
+        return False
+    if (toks[a + 1:] != pad_id).any():
+        return False
+    y = int(toks[a])
+    if not 0 <= y < V:
+        return False
+    T = host["temperature"][b]
+    p = _softmax(_decode(host["target"][first + b + a]), T)
+    if a == s:
+        return p[y] > 0
+    q = _softmax(_decode(host["draft"][first + a]), T)
+    w = np.maximum(p - q, 0.0)
+    if w.sum() <= 1e-12:
+        return p[y] > 0
+    return p[y] - q[y] > -1e-6 * max(p[y], q[y], 1e-30) - 1e-12
+
+
+def compare_verify(got, ref, sl, cu_sl, label="", host=None):
+    """Asserts the comparison rules; returns a small report.  With the host
+    inputs given, tie sequences are also checked to be valid emissions."""
     B = len(sl)
     err_g = got["seq_err"].astype(np.uint32)
     err_r = ref["seq_err"].astype(np.uint32)
@@ -51,6 +95,8 @@ def compare_verify(got, ref, sl, cu_sl, label=""):
         assert 0 <= a <= sl[b]
         toks = got["tokens"][b]
         assert (toks[a + 1:] == -1).all()
+        if host is not None:
+            assert emission_is_valid(got, host, b), f"{label}: tie sequence {b} emits an invalid draw"
     # errored sequences get the defined fallback
     for b in np.nonzero(~fine)[0]:
         assert got["accepted"][b] == 0 and (got["tokens"][b] == -1).all()

@@ -127,3 +127,13 @@ def test_binding_never_touches_the_oracle():
     for f in os.listdir(os.path.join(ROOT, "paper_2509_01083_amd", "csrc")):
         src += open(os.path.join(ROOT, "paper_2509_01083_amd", "csrc", f)).read()
     assert "oracle" not in src.lower()
+
+
+def test_stream_read_rejects_invalid_arguments(lib):
+    fn = lib.dsde_stream_read
+    fn.restype = ctypes.c_int32
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+    ok_buf, out = ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000)
+    for buf, nbytes, o in ((None, 16, out), (ok_buf, 16, None), (ok_buf, 0, out), (ok_buf, -16, out),
+                           (ok_buf, 24, out), (ctypes.c_void_p(0x1008), 16, out)):
+        assert fn(buf, nbytes, o, None) == 1

@@ -157,7 +157,7 @@ def chained_step(dsde, step, st, sl_max, sl_hi, label):
     host = W.host_arrays(step)
     smax = sl_max.cpu().numpy().astype(np.float64)
     ref, sr, nr, spread = oracle_chain(host, h0, hd0, c0, smax, sl_hi)
-    rep = compare_verify(got, ref, host["sl"], host["cu_sl"], label)
+    rep = compare_verify(got, ref, host["sl"], host["cu_sl"], label, host=host)
     kld_t = torch.as_tensor(got["kld"], device="cuda")
     sg = gpu_signal(dsde, step.sl, step.cu_sl, kld_t, st)
     compare_signal(sg, sr, f"{label} signal", spread)
@@ -256,7 +256,44 @@ def test_fused_step_parity(gpu_lib, name):
     host = W.host_arrays(step)
     smax = st.sl_max.cpu().numpy().astype(np.float64)
     ref, sr, nr, spread = oracle_chain(host, h0, hd0, c0, smax, step.k_max)
-    rep = compare_verify(got, ref, host["sl"], host["cu_sl"], f"step {name}")
+    rep = compare_verify(got, ref, host["sl"], host["cu_sl"], f"step {name}", host=host)
     compare_signal({**got, "seq_err": got["seq_err"].astype(np.uint32) & 96}, sr, f"step {name} signal", spread)
     rep["sl_ties"] = compare_sl(got, nr, sr, spread, smax, step.k_max, f"step {name}")
     print(f"[report] fused step {name}: {rep}", flush=True)
+
+
+def test_resume_from_snapshot(gpu_lib):
+    """Checkpoint and resume of the controller state: restarting a run of
+    dsde_step from a copy of (hist, head, count) taken midway, in fresh
+    buffers, reproduces the uninterrupted run bit for bit."""
+    cfg = dict(W.CONFIGS["loop"], B=128, V=4096)
+    seed, steps, cut = 8, 10, 4
+    announce(f"resume B={cfg['B']} V={cfg['V']} {steps} steps, snapshot at {cut}")
+    st = W.make_signal_state(cfg, seed=seed, device="cuda")
+    sl, sigma = W.sample_sl(cfg, seed), W.initial_sigma(cfg, seed)
+
+    def one(st_, t, sl_, sigma_):
+        step = W.make_step(cfg, seed=seed, device="cuda", step=t, sl=sl_, sigma=sigma_)
+        f = gpu_lib.step(step.target, step.draft, step.sl, step.cu_sl, step.draft_tokens, step.temperature,
+                         step.u_acc, step.u_res, step.k_max, st_.hist, st_.head, st_.count, st_.sl_max)
+        torch.cuda.synchronize()
+        return {k: v.clone() for k, v in f.items()}
+
+    full, snap = [], None
+    for t in range(steps):
+        if t == cut:
+            snap = (clone_state(st), sl.copy(), sigma.copy())
+        f = one(st, t, sl, sigma)
+        full.append(f)
+        sl, sigma = f["sl_next"].cpu().numpy(), W.walk_sigma(sigma, cfg, seed, t)
+    st2, sl, sigma = snap
+    for t in range(cut, steps):
+        f = one(st2, t, sl, sigma)
+        for k, v in f.items():
+            a, b = v, full[t][k]
+            if a.dtype.is_floating_point:
+                a, b = a.view(torch.int32), b.view(torch.int32)
+            assert torch.equal(a, b), f"step {t}: {k} differs after resume"
+        sl, sigma = f["sl_next"].cpu().numpy(), W.walk_sigma(sigma, cfg, seed, t)
+    assert torch.equal(st2.hist.view(torch.int32), st.hist.view(torch.int32))
+    assert torch.equal(st2.head, st.head) and torch.equal(st2.count, st.count)

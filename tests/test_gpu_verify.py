@@ -23,7 +23,8 @@ def check_step(dsde, step, label, n_threads=16):
     announce(f"{label}: B={step.B} N={step.N} V={step.V} dtype={step.target.dtype}")
     got = run_verify(dsde, step)
     ref = oracle.verify(**W.host_arrays(step), n_threads=n_threads)
-    rep = compare_verify(got, ref, W.host_arrays(step)["sl"], step.cu_sl.cpu().numpy(), label)
+    host = W.host_arrays(step)
+    rep = compare_verify(got, ref, host["sl"], host["cu_sl"], label, host=host)
     print(f"[report] {label}: {rep}", flush=True)
     return got, ref, rep
 
@@ -203,3 +204,30 @@ def test_draw_distribution_matches_target(gpu_lib):
     dist = np.zeros(V)
     np.add.at(dist, got["tokens"][:, 0], np.asarray(wt))
     np.testing.assert_allclose(dist, p, atol=2.0 / M)
+
+
+def test_constructed_ties(gpu_lib):
+    """Acceptance uniforms set to p(x)/q(x) itself (nearest fp32), and draw
+    uniforms that put u' * Z exactly on a CDF boundary of uniform logits: the
+    oracle flags these as ties; the GPU must emit a valid draw for each, and
+    match the oracle exactly on the interleaved sequences without a tie."""
+    rng = np.random.default_rng(9)
+    V, B = 50, 96
+    sls = [1] * 64 + [0] * 32
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V, noise=0.8)
+    sl, cu = packed_layout(sls)
+    for b in range(0, 64, 2):  # even sequences: u on the acceptance boundary
+        j = cu[b]
+        p = np.exp(target[j + b].astype(np.float64))
+        p /= p.sum()
+        q = np.exp(draft[j].astype(np.float64))
+        q /= q.sum()
+        r = p[tokens[j]] / q[tokens[j]]
+        u_acc[j] = np.float32(min(r, 1.0 - 2.0 ** -24))
+    # bonus draws over uniform logits: C(k) = k/4 exactly for V = 4 tokens
+    tgt = np.vstack([target[:cu[64] + 64], np.zeros((32, V), np.float32)])
+    tgt[cu[64] + 64:, 4:] = -60.0  # only the first four tokens carry mass
+    u_res[64:] = np.tile(np.array([0.25, 0.5, 0.75, 0.3], np.float32), 8)
+    step = step_from_arrays(tgt, draft, sls, tokens, [1.0] * B, u_acc, u_res, 1, "fp32")
+    _, ref, rep = check_step(gpu_lib, step, "constructed ties")
+    assert rep["acc_ties"] >= 24 and rep["cdf_ties"] >= 24, rep
