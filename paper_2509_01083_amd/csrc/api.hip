@@ -11,6 +11,8 @@ hipEvent_t g_prof_start = nullptr, g_prof_stop = nullptr;
 bool verify_sizes_ok(int32_t B, int64_t N, int64_t V, int32_t k_max) {
   if (B < 1 || V < 1 || V > DSDE_MAX_VOCAB || N < 0 || k_max < 0 || k_max > DSDE_MAX_K) return false;
   if (N > int64_t(B) * k_max) return false;
+  // per-sequence slots b * k_max + j index the chunk partials
+  if (int64_t(B) * k_max >= (int64_t(1) << 31)) return false;
   const int64_t nc = (V + dsde::kChunk - 1) / dsde::kChunk;
   // the grid of the statistics pass must fit one launch dimension
   if (N * nc >= (int64_t(1) << 31)) return false;
@@ -40,7 +42,7 @@ const char *dsde_status_string(int32_t status) {
 
 size_t dsde_verify_workspace_bytes(int32_t B, int64_t N, int64_t V, int32_t k_max) {
   if (!verify_sizes_ok(B, N, V, k_max)) return 0;
-  return dsde::workspace_layout(N, V).total;
+  return dsde::workspace_layout(B, N, V, k_max).total;
 }
 
 int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
@@ -55,7 +57,7 @@ int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t
       !workspace)
     return DSDE_INVALID_ARG;
   if (N > 0 && (!draft_logits || !draft_tokens || !u_acc || !kld)) return DSDE_INVALID_ARG;
-  if (workspace_bytes < dsde::workspace_layout(N, V).total) return DSDE_WORKSPACE_TOO_SMALL;
+  if (workspace_bytes < dsde::workspace_layout(B, N, V, k_max).total) return DSDE_WORKSPACE_TOO_SMALL;
   if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return DSDE_INVALID_ARG;
   dsde::VerifyArgs a;
   a.target = target_logits;
@@ -104,7 +106,7 @@ int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t d
   if (!hist || !head || !count || !mu_last || !var_short || !var_long || !wvir || !sf) return DSDE_INVALID_ARG;
   if (!isfinite(sl_min) || ceilf(sl_min) > float(sl_hi)) return DSDE_INVALID_ARG;
   if (!sl_max || !sl_hat || !sl_cap || !sl_next) return DSDE_INVALID_ARG;
-  if (workspace_bytes < dsde::workspace_layout(N, V).total) return DSDE_WORKSPACE_TOO_SMALL;
+  if (workspace_bytes < dsde::workspace_layout(B, N, V, k_max).total) return DSDE_WORKSPACE_TOO_SMALL;
   if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return DSDE_INVALID_ARG;
   dsde::SignalArgs sg;
   sg.hist = hist;

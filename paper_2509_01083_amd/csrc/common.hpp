@@ -19,13 +19,15 @@ constexpr double kLn2 = 0.6931471805599453;
 constexpr float kMinTemp = 1.52587890625e-05f, kMaxTemp = 65536.0f;
 
 // One row pair of the statistics pass, in processing order: the drafted
-// position (pair index), its target row (-1 when the layout is invalid) and
-// the log2-domain scale c = log2(e) / T_b as raw float bits.
+// position (pair index = draft row), its target row (-1 when the layout is
+// invalid), the log2-domain scale c = log2(e) / T_b as raw float bits, and
+// its slot b * k_max + j, under which its chunk partials and gathered logits
+// are stored (so that their address depends on the sequence alone).
 struct WorkItem {
   int32_t pair;
   int32_t target_row;
   uint32_t scale_bits;
-  int32_t pad;
+  int32_t slot;
 };
 
 // Row statistics of one chunk of one drafted row pair, relative to the
@@ -56,17 +58,18 @@ struct WorkspaceLayout {
 
 inline int64_t num_chunks(int64_t V) { return (V + kChunk - 1) / kChunk; }
 
-inline WorkspaceLayout workspace_layout(int64_t N, int64_t V) {
+inline WorkspaceLayout workspace_layout(int32_t B, int64_t N, int64_t V, int32_t k_max) {
   const int64_t nc = num_chunks(V);
   const size_t n = size_t(N > 0 ? N : 1);
+  const size_t slots = size_t(int64_t(B) * k_max > 0 ? int64_t(B) * k_max : 1);
   WorkspaceLayout L;
   size_t off = 0;
   L.work = off;
   off += align_up(sizeof(WorkItem) * n);
   L.pair_chunk = off;
-  off += align_up(sizeof(PairChunk) * n * size_t(nc));
+  off += align_up(sizeof(PairChunk) * slots * size_t(nc));
   L.gathered = off;
-  off += align_up(sizeof(Gathered) * n);
+  off += align_up(sizeof(Gathered) * slots);
   L.total = off;
   return L;
 }

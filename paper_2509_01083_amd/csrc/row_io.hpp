@@ -222,4 +222,12 @@ __device__ __forceinline__ void load_run(const void *row, int64_t V, int64_t sta
   }
 }
 
+// Keeps a prefetched value where it was loaded: an empty asm statement that
+// takes it as an operand (it emits no instruction).  Without it the compiler
+// may sink a load to its first use, past the branches and barriers the
+// prefetch is meant to overlap with.
+__device__ __forceinline__ void pin(float v) { asm volatile("" ::"v"(v)); }
+__device__ __forceinline__ void pin(double v) { asm volatile("" ::"v"(v)); }
+__device__ __forceinline__ void pin(int32_t v) { asm volatile("" ::"v"(v)); }
+
 }  // namespace dsde

@@ -18,7 +18,7 @@ namespace dsde {
 namespace {
 
 constexpr int kSigThreads = 256;  // 4 sequences per workgroup
-constexpr int kCapThreads = 1024;
+constexpr int kCapThreads = 256;
 
 __global__ __launch_bounds__(kSigThreads) void kld_signal_kernel(
     int32_t B, int64_t N, const int32_t *__restrict__ sl, const int32_t *__restrict__ cu_sl,
@@ -57,8 +57,8 @@ __global__ __launch_bounds__(kCapThreads) void next_sl_kernel(int32_t B, const f
                                                               float *__restrict__ sl_cap,
                                                               int32_t *__restrict__ sl_next,
                                                               uint32_t *__restrict__ seq_err, bool or_err) {
-  __shared__ double red_s[kCapThreads];
-  __shared__ int red_n[kCapThreads];
+  __shared__ double red_s[kCapThreads / 64];
+  __shared__ int red_n[kCapThreads / 64];
   block_next_sl(B, sf, wvir, sl_max, sl_min, sl_hi, sl_hat, sl_cap, sl_next, seq_err, or_err, red_s, red_n);
 }
 

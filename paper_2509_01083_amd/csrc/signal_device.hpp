@@ -29,9 +29,13 @@ struct RingPrefetch {
 __device__ __forceinline__ RingPrefetch wave_ring_prefetch(const float *ring, const int32_t *head,
                                                            const int32_t *count, int32_t W) {
   const int lane = threadIdx.x & 63;
+  // mbcnt over an empty mask is 0 in every lane, but the compiler treats it
+  // as lane-varying: head and count become vector loads, issued with the ring
+  // loads, instead of scalar loads competing for scalar registers
+  const uint32_t zero = __builtin_amdgcn_mbcnt_lo(0u, 0u);
   RingPrefetch r;
-  r.head = *head;
-  r.count = *count;
+  r.head = head[zero];
+  r.count = count[zero];
 #pragma unroll
   for (int k = 0; k < kRingRegs; ++k) {
     const int32_t i = lane + 64 * k;
@@ -47,6 +51,7 @@ __device__ __forceinline__ float ring_slot(const RingPrefetch &rp, const float *
     float v = 0.f;
 #pragma unroll
     for (int k = 0; k < kRingRegs; ++k) {
+      if (64 * k >= W) break;  // uniform: registers past the ring hold nothing
       const float x = __shfl(rp.slot[k], slot & 63);
       if ((slot >> 6) == k) v = x;
     }
@@ -189,13 +194,15 @@ __device__ __forceinline__ double sl_hat_of(double sf, double wvir, double sl_ma
   return pen <= 1.0 ? (1.0 - pen) * (sl_max - sl_min) + sl_min : sl_min;
 }
 
-// SL rule and batch cap by one workgroup (any blockDim up to 1024; `red_s`,
-// `red_n` are blockDim-sized LDS arrays).  seq_err bits are OR-ed atomically
-// when `or_err` is set (fused step), else written.
+// SL rule and batch cap by one workgroup (blockDim a multiple of 64, at most
+// 1024; `red_s`, `red_n` are LDS arrays of blockDim / 64 entries).  Per-thread
+// fp64 partial sums, wavefront butterflies, then the wavefront totals in order:
+// a fixed order, so the cap is bitwise reproducible.  seq_err bits are OR-ed
+// atomically when `or_err` is set (fused step), else written.
 __device__ inline void block_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max,
                                      float sl_min, int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next,
                                      uint32_t *seq_err, bool or_err, double *red_s, int *red_n) {
-  const int t = threadIdx.x, nt = blockDim.x;
+  const int t = threadIdx.x, nt = blockDim.x, lane = t & 63, wave = t >> 6;
   const double lo_f = double(sl_min);
   const int32_t lo = int32_t(ceil(lo_f));
   double part = 0.0;
@@ -212,17 +219,21 @@ __device__ inline void block_next_sl(int32_t B, const float *sf, const float *wv
       sl_hat[b] = NAN;
     }
   }
-  red_s[t] = part;
-  red_n[t] = cnt;
-  __syncthreads();
-  for (int o = nt / 2; o > 0; o >>= 1) {
-    if (t < o) {
-      red_s[t] += red_s[t + o];
-      red_n[t] += red_n[t + o];
-    }
-    __syncthreads();
+  part = wave_sum_f64(part);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
+  if (lane == 0) {
+    red_s[wave] = part;
+    red_n[wave] = cnt;
   }
-  const double cap = red_n[0] > 0 ? red_s[0] / double(red_n[0]) : NAN;
+  __syncthreads();
+  double total = 0.0;
+  int n = 0;
+  for (int v = 0; v < nt / 64; ++v) {
+    total += red_s[v];
+    n += red_n[v];
+  }
+  const double cap = n > 0 ? total / double(n) : NAN;
   if (t == 0) sl_cap[0] = float(cap);
   for (int32_t b = t; b < B; b += nt) {
     const double f = sf[b], w = wvir[b], mx = sl_max[b];

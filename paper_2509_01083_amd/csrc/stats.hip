@@ -35,7 +35,7 @@ __global__ __launch_bounds__(1024) void setup_kernel(int32_t B, int64_t N, int32
   if (c_first != 0 || c_last != N) bad = 1;
   if (bad) {
     for (int32_t b = t; b < B; b += blockDim.x) seq_err[b] = DSDE_ERR_LAYOUT;
-    for (int64_t k = t; k < N; k += blockDim.x) work[k] = WorkItem{int32_t(k), -1, 0u, 0};
+    for (int64_t k = t; k < N; k += blockDim.x) work[k] = WorkItem{int32_t(k), -1, 0u, -1};
     return;
   }
   for (int32_t b = t; b < B; b += blockDim.x) {
@@ -44,7 +44,7 @@ __global__ __launch_bounds__(1024) void setup_kernel(int32_t B, int64_t N, int32
     // the same expression as every later kernel's scale; a temperature outside
     // the admissible range is flagged by the acceptance kernel
     const uint32_t cbits = __float_as_uint(kLog2e / temperature[b]);
-    for (int32_t j = 0; j < s; ++j) work[first + j] = WorkItem{first + j, first + b + j, cbits, 0};
+    for (int32_t j = 0; j < s; ++j) work[first + j] = WorkItem{first + j, first + b + j, cbits, b * k_max + j};
   }
 }
 
@@ -126,10 +126,10 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
           a = pick_bf16(rt_, i);
           b = pick_bf16(rd_, i);
         }
-      gathered[w.pair] = Gathered{a, b};
+      gathered[w.slot] = Gathered{a, b};
     }
   }
-  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.pair) * nc + chunk);
+  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.slot) * nc + chunk);
 }
 
 // fp32 rows, or rows without 16-byte alignment.
@@ -182,10 +182,10 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
           a = zt[i];
           b = zd[i];
         }
-      gathered[w.pair] = Gathered{a, b};
+      gathered[w.slot] = Gathered{a, b};
     }
   }
-  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.pair) * nc + chunk);
+  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.slot) * nc + chunk);
 }
 
 }  // namespace

@@ -79,13 +79,13 @@ __device__ __forceinline__ double group_sum(double v) {
   return v;
 }
 
-// Combines the chunk partials of every drafted pair of one sequence: groups of
-// G lanes, one pair per group, lane g of a group folds chunks g, g + G, ...
-// Results go to LDS (st_*[j] for position j).
+// Combines the chunk partials of every drafted pair of one sequence (stored
+// under slots slot0 + j): groups of G lanes, one pair per group, lane g of a
+// group folds chunks g, g + G, ...  Results go to LDS (st_*[j] for position j).
 template <int G>
-__device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t first, int32_t s, int32_t nc,
-                                     float *st_mt, float *st_md, double *st_sp, double *st_sq, double *st_a,
-                                     int *st_bad) {
+__device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t slot0, int32_t s, int32_t nc,
+                                     const PairChunk &q0, float *st_mt, float *st_md, double *st_sp, double *st_sq,
+                                     double *st_a, int *st_bad) {
   constexpr int P = 64 / G;  // pairs per wavefront
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane % G;
   for (int32_t base = 0; base < s; base += kSeqWaves * P) {
@@ -94,7 +94,8 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
     double lsp = 0.0, lsq = 0.0, la = 0.0;
     if (j < s) {
       for (int32_t ch = g; ch < nc; ch += G) {
-        const PairChunk q = part[(first + j) * nc + ch];
+        // the first chunk of the first round was fetched at kernel start
+        const PairChunk q = base == 0 && ch == g ? q0 : part[(slot0 + j) * nc + ch];
         if (lmt == -INFINITY) {
           lmt = q.mt;
           lmd = q.md;
@@ -280,12 +281,41 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
   const int32_t b = blockIdx.x;
   const int32_t width = P.k_max + 1;
   int32_t *tok = P.tokens + int64_t(b) * width;
-  // the signal wavefront fetches the ring state first: it does not depend on
-  // anything this kernel computes
+  // first round trip: everything whose address depends on the sequence index
+  // alone - the ring state (signal wavefront), this sequence's chunk partials
+  // and gathered logits (stored by slot b * k_max + j; positions past SL_b are
+  // fetched and ignored), and the per-sequence inputs
+  // (every wavefront fetches the ring, a few hundred bytes, so that no branch
+  // separates these loads from the rest of the round trip; only the signal
+  // wavefront uses it)
   RingPrefetch rp{};
-  if constexpr (FUSED)
-    if (wave == kSignalWave) rp = wave_ring_prefetch(S.hist + int64_t(b) * S.W, S.head + b, S.count + b, S.W);
+  if constexpr (FUSED) rp = wave_ring_prefetch(S.hist + int64_t(b) * S.W, S.head + b, S.count + b, S.W);
+  const int G = P.nc <= 16 ? 16 : P.nc <= 32 ? 32 : 64;
+  const int32_t j0 = wave * (64 / G) + lane / G, g0 = lane % G;
+  const int64_t slot0 = int64_t(b) * P.k_max;
+  PairChunk q0{};
+  if (j0 < P.k_max && g0 < P.nc) q0 = P.part[(slot0 + j0) * P.nc + g0];
+  Gathered gz{0.f, 0.f};
+  if (wave == 0 && lane < P.k_max) gz = P.gathered[slot0 + lane];
   uint32_t err = P.seq_err[b];  // the set-up's layout verdict
+  const int32_t s = P.sl[b], first = P.cu_sl[b];
+  const float T = P.temperature[b], ur = P.u_res[b];
+  // one wait for the whole first round trip: every load above is issued
+  // before any of the pins below asks for its value
+  asm volatile("" ::: "memory");
+  pin(q0.mt);
+  pin(q0.md);
+  pin(q0.sp);
+  pin(q0.sq);
+  pin(q0.a);
+  pin(gz.zt);
+  pin(gz.zd);
+  if constexpr (FUSED) {
+    pin(rp.head);
+    pin(rp.count);
+#pragma unroll
+    for (int k = 0; k < kRingRegs; ++k) pin(rp.slot[k]);
+  }
   if (err & DSDE_ERR_LAYOUT) {
     if (t < width) tok[t] = P.pad_id;
     if (t == 0) {
@@ -294,29 +324,24 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
     }
     return;
   }
-  const int32_t s = P.sl[b], first = P.cu_sl[b];
-  const float T = P.temperature[b], ur = P.u_res[b];
-  // per-position inputs of wavefront 0 (lane j = drafted position j), fetched
-  // together with the chunk partials below
+  // per-position inputs of wavefront 0 (lane j = drafted position j)
   int32_t x = 0;
   float u = 0.f;
-  Gathered gz{0.f, 0.f};
   if (wave == 0 && lane < s) {
     x = P.draft_tokens[first + lane];
     u = P.u_acc[first + lane];
-    gz = P.gathered[first + lane];
   }
 
   // ---- 1. acceptance
   // row statistics of every drafted pair (read even for a flagged sequence:
   // the layout is valid, so every access stays in bounds)
   if (s > 0) {
-    if (P.nc <= 16)
-      combine_pairs<16>(P.part, first, s, P.nc, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
-    else if (P.nc <= 32)
-      combine_pairs<32>(P.part, first, s, P.nc, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
+    if (G == 16)
+      combine_pairs<16>(P.part, slot0, s, P.nc, q0, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
+    else if (G == 32)
+      combine_pairs<32>(P.part, slot0, s, P.nc, q0, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
     else
-      combine_pairs<64>(P.part, first, s, P.nc, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
+      combine_pairs<64>(P.part, slot0, s, P.nc, q0, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
   }
   __syncthreads();
   if (wave == 0) {
@@ -624,7 +649,7 @@ static void launch_seq(const VerifyArgs &a, const StepParams &P, const SignalArg
 }
 
 int launch_verify(const VerifyArgs &a) {
-  const WorkspaceLayout L = workspace_layout(a.N, a.V);
+  const WorkspaceLayout L = workspace_layout(a.B, a.N, a.V, a.k_max);
   const int32_t nc = int32_t(num_chunks(a.V));
   char *ws = (char *)a.workspace;
   WorkItem *work = (WorkItem *)(ws + L.work);
