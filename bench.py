@@ -60,6 +60,9 @@ def main():
     dsde.load()
     dev = torch.device("cuda:0")
     cfg = W.CONFIGS[args.workload]
+    if args.workload == "loop":
+        print(json.dumps(run_loop(args, cfg, dev)), flush=True)
+        return
     sl = W.sample_sl(cfg, args.seed)
     copies = [W.make_step(cfg, seed=args.seed + i, device=dev, sl=sl) for i in range(2)]
     st = W.make_signal_state(cfg, seed=args.seed, device=dev)
@@ -178,6 +181,8 @@ def main():
         result["stream_read_ceiling"] = {"gbps": ceil_gbps, "bytes": 4 << 30, "launches": reps}
         result["roofline"]["frac_of_stream_ceiling"] = k1_gbps / ceil_gbps
 
+    result["straggler"] = straggler_report(outs[last], k_max)
+
     if not args.no_cpu_baseline:
         result["cpu_baseline"], result["parity"] = cpu_baseline(copies[last], outs[last], st, args.cpu_seconds)
     if args.copy_calibration:
@@ -200,6 +205,110 @@ def _record(ev, stream):
     HipEvent._hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
     if HipEvent._hip.hipEventRecord(ev.handle, ctypes.c_void_p(stream.cuda_stream)) != 0:
         raise RuntimeError("hipEventRecord failed")
+
+
+def straggler_report(out, sl_hi, sl_min=2.0):
+    """Next-step SLs with and without the batch cap (Sec. 3.3): the largest SL,
+    the sum, and the padded-slot waste B * max - sum of a batch padded to its
+    longest sequence (the quantity the cap shrinks)."""
+    import numpy as np
+    hat = out["sl_hat"].cpu().numpy().astype(np.float64)
+    capped = out["sl_next"].cpu().numpy().astype(np.int64)
+    ok = np.isfinite(hat)
+    lo = int(np.ceil(sl_min))
+    uncapped = np.where(ok, np.clip(np.floor(hat + 0.5), lo, sl_hi), lo).astype(np.int64)
+    B = len(capped)
+    rep = {"sl_cap": float(out["sl_cap"].cpu().numpy()[0])}
+    for name, v in (("with_cap", capped), ("without_cap", uncapped)):
+        rep[name] = {"max": int(v.max()), "sum": int(v.sum()), "mean": float(v.mean()),
+                     "padded_waste": int(B * v.max() - v.sum())}
+    return rep
+
+
+def run_loop(args, cfg, dev):
+    """The controller loop: every step's SLs are the previous step's decisions
+    (dsde_step's sl_next), the ring starts empty and carries across steps.
+    Logit rows come from two pre-generated pools at the full length k_max (one
+    per parity of the step); each step gathers its packed rows from them
+    (untimed) and draws fresh acceptance and draw uniforms.  Each dsde_step is
+    timed by its own pair of events."""
+    import numpy as np
+    import torch
+
+    import paper_2509_01083_amd as dsde
+    import workloads as W
+    B, V, k_max = cfg["B"], cfg["V"], cfg["k_max"]
+    steps = args.steps
+    full = np.full(B, k_max, np.int32)
+    sigma = W.initial_sigma(cfg, args.seed)
+    pools = [W.make_step(cfg, seed=args.seed + i, device=dev, sl=full, sigma=sigma) for i in range(2)]
+    st = W.make_signal_state(cfg, seed=args.seed, device=dev)
+    esz = 2 if pools[0].target.dtype == torch.bfloat16 else 4
+    tbuf = torch.empty_like(pools[0].target)
+    dbuf = torch.empty_like(pools[0].draft)
+    ws = dsde.new_workspace(B, B * k_max, V, k_max, device=dev)
+    b_idx = np.arange(B)
+    sl = W.sample_sl(cfg, args.seed)
+    times, mean_sl, caps, min_branch, rows_total, bytes_total = [], [], [], [], 0, 0
+    evs = (HipEvent(), HipEvent())
+    stream = torch.cuda.current_stream()
+    g = torch.Generator(device=dev)
+    g.manual_seed(args.seed)
+    for t in range(args.warmup + steps):
+        pool = pools[t % 2]
+        cu = np.zeros(B + 1, np.int32)
+        cu[1:] = np.cumsum(sl)
+        N = int(cu[-1])
+        seq = np.repeat(b_idx, sl)
+        j = np.arange(N) - cu[:-1][seq]
+        # packed target rows (b, j <= SL_b) from the pool's rows b * (k_max + 1) + j
+        seq_t = np.repeat(b_idx, sl + 1)
+        jt = np.arange(N + B) - (cu[:-1] + b_idx)[seq_t]
+        t_idx = torch.as_tensor(seq_t * (k_max + 1) + jt, device=dev)
+        d_idx = torch.as_tensor(seq * k_max + j, device=dev)
+        torch.index_select(pool.target, 0, t_idx, out=tbuf[:N + B])
+        torch.index_select(pool.draft, 0, d_idx, out=dbuf[:N])
+        toks = pool.draft_tokens[d_idx].contiguous()
+        u_acc = torch.rand(N, generator=g, device=dev)
+        u_res = torch.rand(B, generator=g, device=dev)
+        sl_t = torch.as_tensor(sl, device=dev)
+        cu_t = torch.as_tensor(cu, device=dev)
+        torch.cuda.synchronize()
+        _record(evs[0], stream)
+        out = dsde.step(tbuf[:N + B], dbuf[:N], sl_t, cu_t, toks, pool.temperature, u_acc, u_res, k_max,
+                        st.hist, st.head, st.count, st.sl_max, workspace=ws)
+        _record(evs[1], stream)
+        torch.cuda.synchronize()
+        if t >= args.warmup:
+            times.append(evs[0].elapsed_ms(evs[1]))
+            mean_sl.append(float(sl.mean()))
+            caps.append(float(out["sl_cap"].cpu().numpy()[0]))
+            hat = out["sl_hat"].cpu().numpy()
+            min_branch.append(float(np.mean(hat <= 2.0)))
+            rows_total += 2 * N + B
+            bytes_total += 2 * N * V * esz
+        sl = out["sl_next"].cpu().numpy().astype(np.int32)
+        if t % 50 == 0:
+            print(f"[loop] step {t}: N={N} mean SL {sl.mean():.2f}", file=sys.stderr, flush=True)
+    evs[0].destroy()
+    evs[1].destroy()
+    tms = np.asarray(times)
+    total_s = tms.sum() * 1e-3
+    return {
+        "metric": METRIC, "value": rows_total / total_s, "unit": "rows/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": float(tms.mean()), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if esz == 2 else "fp32", "data": "synthetic",
+        "config": {"workload": "loop", "B": B, "V": V, "k_max": k_max, "W": cfg["W"], "seed": args.seed},
+        "loop": {"ms_per_step": {"mean": float(tms.mean()), "median": float(np.median(tms)),
+                                 "p95": float(np.percentile(tms, 95)), "min": float(tms.min()),
+                                 "max": float(tms.max())},
+                 "drafted_pair_gbps": bytes_total / total_s / 1e9,
+                 "mean_sl": {"first": mean_sl[0], "last": mean_sl[-1], "mean": float(np.mean(mean_sl))},
+                 "sl_cap": {"first": caps[0], "last": caps[-1], "mean": float(np.mean(caps)),
+                            "min": float(np.min(caps)), "max": float(np.max(caps))},
+                 "fraction_in_sl_min_branch": float(np.mean(min_branch)),
+                 "note": "rows gathered from two pre-generated full-length pools; each step timed alone"},
+    }
 
 
 class HipEvent:

@@ -221,6 +221,8 @@ __device__ inline void bonus_chunk(const char *trow, int64_t V, int64_t ch, floa
     }
     *ref_out = ref;
   } else {
+    // first pass: max and min; second pass over the same logits (now in
+    // cache): the exponentials against the chunk reference
 #pragma unroll kVirtUnroll<DT, VEC>
     for (int k = 0; k < kVirt; ++k) {
       float z[kEltsPerThread];
@@ -232,7 +234,6 @@ __device__ inline void bonus_chunk(const char *trow, int64_t V, int64_t ch, floa
       }
     }
     const float ref = wave_max(m) * scale;
-    // second pass over the same logits (now in cache)
 #pragma unroll kVirtUnroll<DT, VEC>
     for (int k = 0; k < kVirt; ++k) {
       float z[kEltsPerThread];
@@ -640,12 +641,44 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
 
 }  // namespace
 
+// Dynamic LDS of more than half a CU's LDS (see launch_seq); 0 when the
+// runtime does not allow it.  Set up once per kernel.
+template <typename K>
+static size_t spread_lds(K kernel) {
+  int dev = 0, lds = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) != hipSuccess ||
+      lds <= 0) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  const size_t bytes = size_t(lds) / 2 + 1;
+  if (hipFuncSetAttribute(reinterpret_cast<const void *>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                          int(bytes)) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return bytes;
+}
+
 template <int DT, bool VEC>
 static void launch_seq(const VerifyArgs &a, const StepParams &P, const SignalArgs &S) {
+  // Two workgroups fit on one CU.  With no more sequences than CUs the
+  // dispatcher could still pair them up on half of the CUs, each pair then
+  // sharing one CU's load bandwidth; reserving more than half of the CU's LDS
+  // per workgroup (unused) places one sequence per CU.
+  static const size_t spread_fused = spread_lds(seq_kernel<DT, VEC, true>);
+  static const size_t spread_plain = spread_lds(seq_kernel<DT, VEC, false>);
+  int dev = 0, ncu = 0;
+  const bool few = hipGetDevice(&dev) == hipSuccess &&
+                   hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+                   a.B <= ncu;
+  (void)hipGetLastError();
+  const dim3 grid(unsigned(a.B)), block(kSeqThreads);
   if (a.signal)
-    seq_kernel<DT, VEC, true><<<dim3(unsigned(a.B)), dim3(kSeqThreads), 0, a.stream>>>(P, S);
+    seq_kernel<DT, VEC, true><<<grid, block, few ? spread_fused : 0, a.stream>>>(P, S);
   else
-    seq_kernel<DT, VEC, false><<<dim3(unsigned(a.B)), dim3(kSeqThreads), 0, a.stream>>>(P, S);
+    seq_kernel<DT, VEC, false><<<grid, block, few ? spread_plain : 0, a.stream>>>(P, S);
 }
 
 int launch_verify(const VerifyArgs &a) {
