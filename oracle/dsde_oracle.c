@@ -28,6 +28,12 @@
  *                        of the predicted lengths).
  *   oracle_calibrate_sl_max -- Eq. 1 (Sec. 3.1.1).
  *
+ * Greedy verification (the temperature-0.0 setting of the experiments, Sec. 4.2
+ * and Table 3(a)): a sequence with T_b = 0 accepts a drafted token iff it is
+ * the argmax of its target row (the smallest token id among equal maxima) and
+ * emits the argmax of the first rejected row, or of the bonus row; its KLD is
+ * taken on the T = 1 softmaxes, and its uniforms are not used.
+ *
  * Readings where the paper is silent (each is listed with its reason in the
  * design notes of the repository):
  *   - KL direction KL(p_target || q_draft); both softmaxes use the sequence's
@@ -97,6 +103,20 @@ static double row_lse(const void *base, int dtype, int64_t V, int64_t row, doubl
   return m + log(S);
 }
 
+/* The smallest token id holding the row's largest logit. */
+static int64_t row_argmax(const void *base, int dtype, int64_t V, int64_t row) {
+  int64_t best = 0;
+  double m = logit(base, dtype, V, row, 0);
+  for (int64_t v = 1; v < V; ++v) {
+    double z = logit(base, dtype, V, row, v);
+    if (z > m) {
+      m = z;
+      best = v;
+    }
+  }
+  return best;
+}
+
 /* ------------------------------------------------------------------ */
 /* verification step                                                   */
 /* ------------------------------------------------------------------ */
@@ -137,20 +157,22 @@ static void verify_sequence(const verify_job *J, int32_t b) {
   }
   const int64_t first = J->cu_sl[b];          /* first drafted position of b */
   const int64_t trow0 = first + b;            /* its first target row */
-  const double T = (double)J->temperature[b];
+  /* T_b = 0: greedy verification, whose KLD is taken at T = 1 */
+  const int greedy = J->temperature[b] == 0.0f;
+  const double T = greedy ? 1.0 : (double)J->temperature[b];
 
   for (int32_t j = 0; j < SL; ++j) {
     int32_t x = J->draft_tokens[first + j];
     if (x < 0 || (int64_t)x >= V) err |= ORC_BAD_TOKEN;
     float u = J->u_acc[first + j];
-    if (!(u >= 0.0f && u < 1.0f)) err |= ORC_BAD_UNIFORM;
+    if (!greedy && !(u >= 0.0f && u < 1.0f)) err |= ORC_BAD_UNIFORM;
   }
-  {
+  if (!greedy) {
     float u = J->u_res[b];
     if (!(u >= 0.0f && u < 1.0f)) err |= ORC_BAD_UNIFORM;
+    /* the admissible temperature range of the boundary: [2^-16, 2^16] */
+    if (!(T >= ldexp(1.0, -16) && T <= ldexp(1.0, 16))) err |= ORC_BAD_TEMP;
   }
-  /* the admissible temperature range of the boundary: [2^-16, 2^16] */
-  if (!(T >= ldexp(1.0, -16) && T <= ldexp(1.0, 16))) err |= ORC_BAD_TEMP;
   if (!err) {
     for (int32_t j = 0; j < SL; ++j)
       if (!row_is_finite(J->target, J->dtype, V, trow0 + j) ||
@@ -179,6 +201,24 @@ static void verify_sequence(const verify_job *J, int32_t b) {
       J->lse[2 * (first + j)] = lse_p[j];
       J->lse[2 * (first + j) + 1] = lse_q[j];
     }
+  }
+
+  if (greedy) {
+    /* accept x_j while it is the argmax of its target row; emit the argmax of
+     * the first rejected row, or of the bonus row */
+    int32_t a = 0;
+    while (a < SL && (int64_t)J->draft_tokens[first + a] == row_argmax(J->target, J->dtype, V, trow0 + a)) ++a;
+    free(lse_p);
+    free(lse_q);
+    if (a == SL && !row_is_finite(J->target, J->dtype, V, trow0 + SL)) {
+      J->seq_err[b] = ORC_BAD_LOGIT;
+      return;
+    }
+    for (int32_t j = 0; j < a; ++j) tok[j] = J->draft_tokens[first + j];
+    tok[a] = (int32_t)row_argmax(J->target, J->dtype, V, trow0 + a);
+    J->accepted[b] = a;
+    J->seq_err[b] = 0;
+    return;
   }
 
   /* acceptance scan: accept drafted token x_j while u_j < min(1, p(x_j)/q(x_j)) */

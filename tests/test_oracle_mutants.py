@@ -35,6 +35,11 @@ MUTANTS = {
     "sl_hat_branch": ("if (pen <= 1.0) return (1.0 - pen) * (sl_max - sl_min) + sl_min;",
                       "if (pen <= 1.0) return (1.0 - pen) * sl_max + sl_min;"),
     "push_skipped": ("ring[head[b]] = mu;", "(void)0;"),
+    "greedy_tie_takes_last": ("    if (z > m) {\n      m = z;\n      best = v;", "    if (z >= m) {\n      m = z;\n      best = v;"),
+    "greedy_emits_next_row": ("tok[a] = (int32_t)row_argmax(J->target, J->dtype, V, trow0 + a);",
+                              "tok[a] = (int32_t)row_argmax(J->target, J->dtype, V, trow0 + a + (a < SL));"),
+    "greedy_kld_at_zero_scale": ("const double T = greedy ? 1.0 : (double)J->temperature[b];",
+                                 "const double T = greedy ? 2.0 : (double)J->temperature[b];"),
 }
 
 

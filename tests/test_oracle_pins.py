@@ -273,7 +273,7 @@ def test_error_bits_and_fallback_outputs(orc):
     kw = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in base.items()}
     kw["draft_tokens"][2] = 16           # seq 1: token out of range
     kw["u_acc"][4] = 1.0                 # seq 2: uniform not in [0, 1)
-    kw["temperature"][3] = 0.0           # seq 3: temperature
+    kw["temperature"][3] = -1.0          # seq 3: temperature (0 would select greedy verification)
     kw["draft"][8, 5] = np.nan           # seq 4: non-finite logit in a pair
     kw["u_acc"][10:12] = 0.9999          # seq 5: force acceptance of both ...
     kw["target"][5 * 3:5 * 3 + 2] = kw["draft"][10:12]  # ... by equal rows
@@ -440,3 +440,94 @@ def test_sl_tie_analysis(orc):
     assert dh[0] == 0.0
     hat3, dh3 = orc.sl_hat_spread(h[None, :], [head], [cnt], [8.0], [0], rho=1e-4)
     assert hat3[0] == hat2[0] and dh3[0] > 0.0
+
+
+# ---------------------------------------------------------------------------
+# greedy verification (T_b = 0; the temperature-0.0 setting of Sec. 4.2 and
+# Table 3(a))
+# ---------------------------------------------------------------------------
+
+def _greedy_batch(rng, sls, V, gap=3.0):
+    """Random rows whose maxima are unique by at least `gap`."""
+    kw = _random_batch(rng, sls, V, T=0.0)
+    for rows in (kw["target"], kw["draft"]):
+        for r in range(rows.shape[0]):
+            rows[r, rng.integers(0, V)] = rows[r].max() + gap
+    return kw
+
+
+def test_greedy_accepts_the_argmax_prefix_and_emits_the_argmax(orc):
+    rng = np.random.default_rng(41)
+    sls = [4, 3, 2, 0]
+    V = 30
+    kw = _greedy_batch(rng, sls, V)
+    cu = kw["cu_sl"]
+    am = lambda r: int(np.argmax(kw["target"][r]))
+    # seq 0 accepts 2 drafts, seq 1 all 3, seq 2 none, seq 3 drafted nothing
+    for b, acc in ((0, 2), (1, 3), (2, 0)):
+        for j in range(sls[b]):
+            t = am(cu[b] + b + j)
+            kw["draft_tokens"][cu[b] + j] = t if j < acc else (t + 1) % V
+    out = orc.verify(**kw)
+    assert list(out["seq_err"]) == [0, 0, 0, 0]
+    for b, acc in ((0, 2), (1, 3), (2, 0), (3, 0)):
+        assert out["accepted"][b] == acc
+        toks = out["tokens"][b]
+        assert list(toks[:acc]) == list(kw["draft_tokens"][cu[b]: cu[b] + acc])
+        assert toks[acc] == am(cu[b] + b + acc)  # the first rejected row, or the bonus row
+        assert (toks[acc + 1:] == -1).all()
+
+
+def test_greedy_ties_take_the_smallest_token(orc):
+    rng = np.random.default_rng(42)
+    V = 20
+    kw = _random_batch(rng, [1, 1], V, T=0.0)
+    for r in range(kw["target"].shape[0]):
+        m = kw["target"][r].max() + 1.0
+        kw["target"][r, [3, 7, 11]] = m  # three equal maxima
+    kw["draft_tokens"][:] = [7, 3]       # seq 0 drafts a tied maximum that is not the smallest
+    out = orc.verify(**kw)
+    assert list(out["accepted"]) == [0, 1]
+    assert out["tokens"][0][0] == 3 and list(out["tokens"][1][:2]) == [3, 3]
+
+
+def test_greedy_is_the_zero_temperature_limit_of_sampling(orc):
+    """With unique maxima and drafts drawn from q (at T -> 0: the draft row's
+    argmax), sampling at T = 2^-16 accepts exactly the drafts that are the
+    target argmax and draws the target argmax, whatever the uniforms."""
+    rng = np.random.default_rng(43)
+    sls = [3, 1, 4, 2, 0, 5]
+    V = 40
+    kw = _random_batch(rng, sls, V, T=0.0)
+    cu = kw["cu_sl"]
+    tgt, dft = kw["target"], kw["draft"]
+    for r in range(tgt.shape[0]):
+        tgt[r, rng.integers(0, V)] = tgt[r].max() + 3.0
+    for b, s in enumerate(sls):
+        acc = int(rng.integers(0, s + 1))
+        for j in range(s):
+            t = int(np.argmax(tgt[cu[b] + b + j]))
+            x = t if j < acc else int((t + 1 + rng.integers(0, V - 1)) % V)  # x != t after the prefix
+            dft[cu[b] + j, x] = max(dft[cu[b] + j].max(), tgt[cu[b] + b + j].max()) + 3.0
+            kw["draft_tokens"][cu[b] + j] = x
+    greedy = orc.verify(**kw)
+    cold = dict(kw, temperature=np.full(len(sls), 2.0 ** -16, np.float32))
+    for trial in range(4):
+        cold["u_acc"] = rng.random(len(kw["u_acc"])).astype(np.float32)
+        cold["u_res"] = rng.random(len(sls)).astype(np.float32)
+        out = orc.verify(**cold)
+        assert np.array_equal(out["accepted"], greedy["accepted"])
+        assert np.array_equal(out["tokens"], greedy["tokens"])
+
+
+def test_greedy_kld_is_taken_at_unit_temperature_and_uniforms_are_unused(orc):
+    rng = np.random.default_rng(44)
+    sls = [2, 3]
+    kw = _greedy_batch(rng, sls, 25)
+    kw["u_acc"][:] = 1.5   # outside [0, 1): irrelevant for greedy sequences
+    kw["u_res"][:] = -1.0
+    g = orc.verify(**kw)
+    assert list(g["seq_err"]) == [0, 0]
+    unit = orc.verify(**dict(kw, temperature=np.ones(2, np.float32),
+                             u_acc=np.zeros(5, np.float32), u_res=np.zeros(2, np.float32)))
+    np.testing.assert_array_equal(g["kld"], unit["kld"])
