@@ -73,7 +73,7 @@ extern "C" {
 #define DSDE_ERR_TOKEN 2u    /* a drafted token outside [0, V) */
 #define DSDE_ERR_LOGIT 4u    /* NaN or +-inf in a row the step reads (every drafted pair; the bonus row
                                 only when it is sampled) */
-#define DSDE_ERR_TEMP 8u     /* temperature not finite or outside [2^-16, 2^16] */
+#define DSDE_ERR_TEMP 8u     /* temperature neither 0 nor in [2^-16, 2^16] */
 #define DSDE_ERR_UNIFORM 16u /* a uniform outside [0, 1) */
 #define DSDE_ERR_SIGNAL 32u  /* non-finite KLD, SF, WVIR or SL_max, or SL_max < sl_min */
 #define DSDE_ERR_STATE 64u   /* ring head outside [0, W) or count outside [0, W] */
@@ -107,8 +107,10 @@ size_t dsde_verify_workspace_bytes(int32_t B, int64_t N, int64_t V, int32_t k_ma
  *                                        0 <= k_max <= DSDE_MAX_K)
  *   sl [B], cu_sl [B+1]     int32       per-sequence SL and its exclusive prefix sums
  *   draft_tokens [N]        int32       the drafted token at each position
- *   temperature [B]         float       per-sequence sampling temperature T_b in [2^-16, 2^16];
- *                                       p = softmax(z_target / T_b), q = softmax(z_draft / T_b)
+ *   temperature [B]         float       per-sequence temperature T_b: in [2^-16, 2^16] for
+ *                                       speculative sampling with p = softmax(z_target / T_b),
+ *                                       q = softmax(z_draft / T_b); T_b = 0 selects greedy
+ *                                       verification (below); anything else is DSDE_ERR_TEMP
  *   u_acc [N]               float       acceptance uniforms in [0, 1), one per position
  *   u_res [B]               float       draw uniforms in [0, 1), one per sequence
  *   pad_id                              token written into unused slots
@@ -122,6 +124,11 @@ size_t dsde_verify_workspace_bytes(int32_t B, int64_t N, int64_t V, int32_t k_ma
  * The draw walks token ids in ascending order and returns the smallest id whose
  * cumulative weight exceeds u_res[b] times the total weight.  Acceptance is
  * evaluated as u < p(x)/q(x) in double precision.
+ * Greedy verification (T_b = 0; the temperature-0.0 setting of Sec. 4.2): a
+ * drafted token is accepted iff it is the argmax of its target row (the
+ * smallest token id among equal maxima), the argmax of the first rejected row
+ * or of the bonus row is emitted, u_acc and u_res of the sequence are not read
+ * for decisions (nor checked), and kld and row_lse are taken at T = 1.
  */
 int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
                     int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl,

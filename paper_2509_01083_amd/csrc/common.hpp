@@ -23,6 +23,10 @@ constexpr float kMinTemp = 1.52587890625e-05f, kMaxTemp = 65536.0f;
 // invalid), the log2-domain scale c = log2(e) / T_b as raw float bits, and
 // its slot b * k_max + j, under which its chunk partials and gathered logits
 // are stored (so that their address depends on the sequence alone).
+// Sign bit of WorkItem::scale_bits: a greedy pair (T_b = 0), whose chunk
+// argmax of the target row is also wanted.
+constexpr uint32_t kGreedyBit = 0x80000000u;
+
 struct WorkItem {
   int32_t pair;
   int32_t target_row;
@@ -39,6 +43,13 @@ struct alignas(16) PairChunk {
   double sp, sq, a;
 };
 
+// Greedy pairs: the target row's largest logit in a chunk (raw, unscaled) and
+// the smallest token id holding it.
+struct ChunkArg {
+  float zmax;
+  int32_t idx;
+};
+
 // The target and draft logits at the drafted token, captured by the chunk
 // that holds it.
 struct Gathered {
@@ -53,7 +64,7 @@ static_assert(int64_t(kMaxChunks) * kChunk == DSDE_MAX_VOCAB, "vocabulary limit 
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct WorkspaceLayout {
-  size_t work, pair_chunk, gathered, total;
+  size_t work, pair_chunk, gathered, chunk_arg, total;
 };
 
 inline int64_t num_chunks(int64_t V) { return (V + kChunk - 1) / kChunk; }
@@ -70,6 +81,8 @@ inline WorkspaceLayout workspace_layout(int32_t B, int64_t N, int64_t V, int32_t
   off += align_up(sizeof(PairChunk) * slots * size_t(nc));
   L.gathered = off;
   off += align_up(sizeof(Gathered) * slots);
+  L.chunk_arg = off;
+  off += align_up(sizeof(ChunkArg) * slots * size_t(nc));
   L.total = off;
   return L;
 }
@@ -111,7 +124,7 @@ struct VerifyArgs {
 
 int launch_verify(const VerifyArgs &a);
 // The set-up and statistics kernels of one verification step (stats.hip).
-void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gathered *gath);
+void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gathered *gath, ChunkArg *chunk_arg);
 // Rows are 16-byte aligned and V a multiple of the vector width.
 bool rows_vectorizable(const VerifyArgs &a);
 int launch_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu_sl, const float *kld,

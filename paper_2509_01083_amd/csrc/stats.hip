@@ -42,8 +42,11 @@ __global__ __launch_bounds__(1024) void setup_kernel(int32_t B, int64_t N, int32
     const int32_t first = cu_sl[b], s = sl[b];
     seq_err[b] = 0u;
     // the same expression as every later kernel's scale; a temperature outside
-    // the admissible range is flagged by the acceptance kernel
-    const uint32_t cbits = __float_as_uint(kLog2e / temperature[b]);
+    // the admissible range is flagged by the acceptance kernel.  T = 0 selects
+    // greedy verification: statistics at T = 1, and the sign bit asks the
+    // statistics kernel for the chunk argmax of the target row.
+    const float T = temperature[b];
+    const uint32_t cbits = T == 0.0f ? (__float_as_uint(kLog2e) | kGreedyBit) : __float_as_uint(kLog2e / T);
     for (int32_t j = 0; j < s; ++j) work[first + j] = WorkItem{first + j, first + b + j, cbits, b * k_max + j};
   }
 }
@@ -80,21 +83,51 @@ __device__ __forceinline__ void write_pair_chunk(float rt, float rd, float sp, f
   }
 }
 
+// Greedy pairs: the chunk maximum M of the target row and the smallest token
+// id of the chunk holding it, written to *out (one per chunk).  `z(i)` is slot
+// i of this thread's logits.
+template <int DT, bool VEC, typename Z>
+__device__ __forceinline__ void write_chunk_argmax(float M, Z z, int64_t chunk, ChunkArg *out, uint32_t *red) {
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  uint32_t best = 0xffffffffu;
+#pragma unroll
+  for (int i = 0; i < kEltsPerThread; ++i) {
+    const uint32_t idx = uint32_t(Layout<DT, VEC>::index(chunk, i, t));
+    if (z(i) == M && idx < best) best = idx;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t y = __shfl_xor(best, o);
+    best = y < best ? y : best;
+  }
+  if (lane == 0) red[wave] = best;
+  __syncthreads();
+  if (t == 0) {
+    uint32_t m = red[0];
+#pragma unroll
+    for (int v = 1; v < kWaves; ++v) m = red[v] < m ? red[v] : m;
+    *out = ChunkArg{M, int32_t(m)};
+  }
+}
+
 // bf16 rows with 16-byte alignment: the hot kernel.
 __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__restrict__ target,
                                                              const void *__restrict__ draft, int64_t V, int32_t nc,
                                                              const WorkItem *__restrict__ work,
                                                              const int32_t *__restrict__ draft_tokens,
                                                              PairChunk *__restrict__ out,
-                                                             Gathered *__restrict__ gathered) {
+                                                             Gathered *__restrict__ gathered,
+                                                             ChunkArg *__restrict__ chunk_arg) {
   __shared__ float red[5][kWaves];
+  __shared__ uint32_t red_arg[kWaves];
   const int64_t unit = blockIdx.x;
   const int64_t k = unit / nc;
   const int64_t chunk = unit - k * nc;
   const WorkItem w = work[k];
   if (w.target_row < 0) return;
   const int t = threadIdx.x;
-  const float c = __uint_as_float(w.scale_bits);
+  const bool greedy = (w.scale_bits & kGreedyBit) != 0;
+  const float c = __uint_as_float(w.scale_bits & ~kGreedyBit);
   const char *trow = (const char *)target + size_t(w.target_row) * size_t(V) * 2;
   const char *drow = (const char *)draft + size_t(w.pair) * size_t(V) * 2;
   const RawBf16 rt_ = load_raw_bf16(trow, V, chunk, t);
@@ -103,6 +136,9 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
   // chunk maxima -> the reference shifts every exponential of the chunk uses
   const float Mt = block_max(raw_max(rt_), red[0]);
   const float Md = block_max(raw_max(rd_), red[1]);
+  if (greedy)
+    write_chunk_argmax<DSDE_BF16, true>(Mt, [&](int i) { return pick_bf16(rt_, i); }, chunk,
+                                        chunk_arg + int64_t(w.slot) * nc + chunk, red_arg);
   const float rt = Mt * c, rd = Md * c;
   float s[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   acc_vec(rt_.v0, rd_.v0, c, rt, rd, s);
@@ -139,15 +175,18 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
                                                                 int32_t nc, const WorkItem *__restrict__ work,
                                                                 const int32_t *__restrict__ draft_tokens,
                                                                 PairChunk *__restrict__ out,
-                                                                Gathered *__restrict__ gathered) {
+                                                                Gathered *__restrict__ gathered,
+                                                                ChunkArg *__restrict__ chunk_arg) {
   __shared__ float red[5][kWaves];
+  __shared__ uint32_t red_arg[kWaves];
   const int64_t unit = blockIdx.x;
   const int64_t k = unit / nc;
   const int64_t chunk = unit - k * nc;
   const WorkItem w = work[k];
   if (w.target_row < 0) return;
   const int t = threadIdx.x;
-  const float c = __uint_as_float(w.scale_bits);
+  const bool greedy = (w.scale_bits & kGreedyBit) != 0;
+  const float c = __uint_as_float(w.scale_bits & ~kGreedyBit);
   const size_t esz = DT == DSDE_BF16 ? 2 : 4;
   const char *trow = (const char *)target + size_t(w.target_row) * size_t(V) * esz;
   const char *drow = (const char *)draft + size_t(w.pair) * size_t(V) * esz;
@@ -162,6 +201,9 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
   }
   const float Mt = block_max(mt, red[0]);
   const float Md = block_max(md, red[1]);
+  if (greedy)
+    write_chunk_argmax<DT, VEC>(Mt, [&](int i) { return zt[i]; }, chunk, chunk_arg + int64_t(w.slot) * nc + chunk,
+                                red_arg);
   const float rt = Mt * c, rd = Md * c;
   float s[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -210,7 +252,7 @@ bool rows_vectorizable(const VerifyArgs &a) {
          (a.dtype == DSDE_BF16 ? a.V % 8 == 0 : a.V % 4 == 0);
 }
 
-void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gathered *gath) {
+void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gathered *gath, ChunkArg *chunk_arg) {
   const int32_t nc = int32_t(num_chunks(a.V));
   const bool prof = a.prof_start && a.prof_stop && a.N > 0;
   launch_timed(setup_kernel, dim3(1), dim3(1024), a.stream, prof ? a.prof_start : nullptr, a.B, a.N, a.k_max,
@@ -224,16 +266,16 @@ void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gat
   const int32_t *tokens = a.draft_tokens;
   const WorkItem *w = work;
   if (a.dtype == DSDE_BF16 && vec)
-    launch_timed(stats_kernel_bf16, grid, block, a.stream, done, T, D, V, nc, w, tokens, part, gath);
+    launch_timed(stats_kernel_bf16, grid, block, a.stream, done, T, D, V, nc, w, tokens, part, gath, chunk_arg);
   else if (a.dtype == DSDE_BF16)
     launch_timed(stats_kernel_generic<DSDE_BF16, false>, grid, block, a.stream, done, T, D, V, nc, w, tokens, part,
-                 gath);
+                 gath, chunk_arg);
   else if (vec)
     launch_timed(stats_kernel_generic<DSDE_FP32, true>, grid, block, a.stream, done, T, D, V, nc, w, tokens, part,
-                 gath);
+                 gath, chunk_arg);
   else
     launch_timed(stats_kernel_generic<DSDE_FP32, false>, grid, block, a.stream, done, T, D, V, nc, w, tokens, part,
-                 gath);
+                 gath, chunk_arg);
 }
 
 }  // namespace dsde

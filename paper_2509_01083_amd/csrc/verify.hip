@@ -51,11 +51,13 @@ struct StepParams {
   double *row_lse;
   const PairChunk *part;
   const Gathered *gathered;
+  const ChunkArg *chunk_arg;  // greedy pairs: the target row's maximum and argmax per chunk
 };
 
 // What the draw of one sequence needs, decided by the acceptance.
 struct DrawJob {
-  int32_t kind;          // 0: residual of the first rejected pair, 1: bonus row, -1: nothing (flagged)
+  int32_t kind;          // 0: residual of the first rejected pair, 1: bonus row, 2: greedy, token known,
+                         // 3: greedy, argmax of the bonus row, -1: nothing (flagged)
   int32_t accepted;      // a_b
   int32_t target_row;
   int32_t draft_row;     // -1 for the bonus row
@@ -63,6 +65,7 @@ struct DrawJob {
   float mt, md;          // row reference shifts of the rejected pair
   float inv_sp, inv_sq;  // 1 / row sums of the rejected pair
   float u;               // draw uniform
+  int32_t token;         // greedy: the emitted token when it is already known
 };
 
 // xor-butterfly reductions inside aligned groups of G lanes (G a power of two)
@@ -84,18 +87,31 @@ __device__ __forceinline__ double group_sum(double v) {
 // group folds chunks g, g + G, ...  Results go to LDS (st_*[j] for position j).
 template <int G>
 __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t slot0, int32_t s, int32_t nc,
-                                     const PairChunk &q0, float *st_mt, float *st_md, double *st_sp, double *st_sq,
-                                     double *st_a, int *st_bad) {
+                                     const PairChunk &q0, const ChunkArg *__restrict__ chunk_arg, ChunkArg arg0,
+                                     float *st_mt, float *st_md, double *st_sp, double *st_sq, double *st_a,
+                                     int *st_bad, int *st_arg) {
   constexpr int P = 64 / G;  // pairs per wavefront
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane % G;
   for (int32_t base = 0; base < s; base += kSeqWaves * P) {
     const int32_t j = base + wave * P + lane / G;
     float lmt = -INFINITY, lmd = -INFINITY;
     double lsp = 0.0, lsq = 0.0, la = 0.0;
+    // greedy: the largest raw logit among this lane's chunks and its token
+    float lz = -INFINITY;
+    int32_t larg = 0x7fffffff;
     if (j < s) {
       for (int32_t ch = g; ch < nc; ch += G) {
         // the first chunk of the first round was fetched at kernel start
-        const PairChunk q = base == 0 && ch == g ? q0 : part[(slot0 + j) * nc + ch];
+        const bool pre = base == 0 && ch == g;
+        const PairChunk q = pre ? q0 : part[(slot0 + j) * nc + ch];
+        if (chunk_arg) {
+          const ChunkArg qa = pre ? arg0 : chunk_arg[(slot0 + j) * nc + ch];
+          // chunks come in ascending order: on equal maxima the earlier wins
+          if (larg == 0x7fffffff || qa.zmax > lz) {
+            lz = qa.zmax;
+            larg = qa.idx;
+          }
+        }
         if (lmt == -INFINITY) {
           lmt = q.mt;
           lmd = q.md;
@@ -127,6 +143,13 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
     tsp = group_sum<G>(tsp);
     tsq = group_sum<G>(tsq);
     ta = group_sum<G>(ta);
+    int32_t arg = 0x7fffffff;
+    if (chunk_arg) {  // the row argmax: smallest token among the chunks holding the row maximum
+      const float zm = group_max<G>(lz);
+      arg = larg != 0x7fffffff && lz == zm ? larg : 0x7fffffff;
+#pragma unroll
+      for (int o = G / 2; o > 0; o >>= 1) arg = min(arg, __shfl_xor(arg, o));
+    }
     if (j < s && g == 0) {
       st_mt[j] = mt;
       st_md[j] = md;
@@ -134,6 +157,7 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
       st_sq[j] = tsq;
       st_a[j] = ta;
       st_bad[j] = !(isfinite(mt) && isfinite(md) && isfinite(tsp) && isfinite(tsq) && isfinite(ta));
+      st_arg[j] = arg;
     }
   }
 }
@@ -254,6 +278,82 @@ __device__ inline void bonus_chunk(const char *trow, int64_t V, int64_t ch, floa
 }
 
 
+// Greedy bonus row, one chunk, by one wavefront: the largest raw logit, the
+// smallest token id holding it, and whether a NaN or +-inf logit was seen.
+template <int DT, bool VEC>
+__device__ inline void bonus_argmax_chunk(const char *trow, int64_t V, int64_t ch, float *zmax_out, int32_t *idx_out,
+                                          int *bad_out) {
+  const int lane = threadIdx.x & 63;
+  if constexpr (VEC && DT == DSDE_BF16) {
+    // pass 1 over the raw chunk in registers: max, min, and a sum that a NaN
+    // propagates through (|z| <= 2^64 keeps finite sums finite); pass 2: the
+    // lanes holding the maximum find its first token (slots of one
+    // chunk-layout thread ascend in token order)
+    RawBf16 r[kVirt];
+#pragma unroll
+    for (int k = 0; k < kVirt; ++k) r[k] = load_raw_bf16(trow, V, ch, lane + 64 * k);
+    float m = -INFINITY, lo = INFINITY, sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < kVirt; ++k)
+#pragma unroll
+      for (int i = 0; i < kEltsPerThread; ++i) {
+        const float z = pick_bf16(r[k], i);
+        m = fmaxf(m, z);
+        lo = fminf(lo, z);
+        sum += z;
+      }
+    const float M = wave_max(m);
+    uint32_t best = 0xffffffffu;
+    if (m == M) {
+#pragma unroll
+      for (int k = 0; k < kVirt; ++k)
+#pragma unroll
+        for (int i = kEltsPerThread - 1; i >= 0; --i)
+          if (pick_bf16(r[k], i) == M) {
+            const uint32_t idx = uint32_t(Layout<DT, VEC>::index(ch, i, lane + 64 * k));
+            best = idx < best ? idx : best;
+          }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint32_t y = __shfl_xor(best, o);
+      best = y < best ? y : best;
+    }
+    *zmax_out = M;
+    *idx_out = int32_t(best);
+    *bad_out = __ballot(m == INFINITY || lo == -INFINITY || sum != sum) != 0;
+  } else {
+    float m = -INFINITY;
+    uint32_t best = 0xffffffffu;
+    int bad = 0;
+#pragma unroll kVirtUnroll<DT, VEC>
+    for (int k = 0; k < kVirt; ++k) {
+      float z[kEltsPerThread];
+      load_chunk_f32<DT, VEC>(trow, V, ch, lane + 64 * k, z);
+#pragma unroll
+      for (int i = 0; i < kEltsPerThread; ++i) {
+        const float v = z[i];  // padding is finite and below every admissible logit
+        if (!isfinite(v)) bad = 1;
+        const uint32_t idx = uint32_t(Layout<DT, VEC>::index(ch, i, lane + 64 * k));
+        if (v > m || (v == m && idx < best)) {
+          m = v;
+          best = idx;
+        }
+      }
+    }
+    const float M = wave_max(m);
+    uint32_t cand = m == M ? best : 0xffffffffu;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint32_t y = __shfl_xor(cand, o);
+      cand = y < cand ? y : cand;
+    }
+    *zmax_out = M;
+    *idx_out = int32_t(cand);
+    *bad_out = __ballot(bad) != 0;
+  }
+}
+
 // One workgroup per sequence.
 //   1. all wavefronts: combine the chunk partials of the drafted pairs (fp64);
 //      wavefront 0: input checks, KLD, acceptance u < p(x)/q(x) (fp64), the
@@ -267,11 +367,12 @@ template <int DT, bool VEC, bool FUSED>
 __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, const SignalArgs S) {
   __shared__ float st_mt[DSDE_MAX_K + 1], st_md[DSDE_MAX_K + 1];
   __shared__ double st_sp[DSDE_MAX_K + 1], st_sq[DSDE_MAX_K + 1], st_a[DSDE_MAX_K + 1];
-  __shared__ int st_bad[DSDE_MAX_K + 1];
+  __shared__ int st_bad[DSDE_MAX_K + 1], st_arg[DSDE_MAX_K + 1];
   __shared__ float s_kld[64];
   __shared__ double ch_w[kMaxChunks], ch_p[kMaxChunks];
   __shared__ float ch_ref[kMaxChunks];
   __shared__ int ch_bad[kMaxChunks];
+  __shared__ int32_t ch_arg[kMaxChunks];
   __shared__ DrawJob s_job;
   __shared__ int32_t s_chunk, s_mode, s_bad;
   __shared__ double s_rem;
@@ -296,6 +397,8 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
   const int64_t slot0 = int64_t(b) * P.k_max;
   PairChunk q0{};
   if (j0 < P.k_max && g0 < P.nc) q0 = P.part[(slot0 + j0) * P.nc + g0];
+  ChunkArg arg0{0.f, 0};  // greedy pairs only; fetched regardless, it costs no extra round trip
+  if (j0 < P.k_max && g0 < P.nc) arg0 = P.chunk_arg[(slot0 + j0) * P.nc + g0];
   Gathered gz{0.f, 0.f};
   if (wave == 0 && lane < P.k_max) gz = P.gathered[slot0 + lane];
   uint32_t err = P.seq_err[b];  // the set-up's layout verdict
@@ -311,6 +414,8 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
   pin(q0.a);
   pin(gz.zt);
   pin(gz.zd);
+  pin(arg0.zmax);
+  pin(arg0.idx);
   if constexpr (FUSED) {
     pin(rp.head);
     pin(rp.count);
@@ -325,6 +430,9 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
     }
     return;
   }
+  // T_b = 0: greedy verification (statistics at T = 1, uniforms unused)
+  const bool greedy = T == 0.0f;
+  const ChunkArg *cargs = greedy ? P.chunk_arg : nullptr;
   // per-position inputs of wavefront 0 (lane j = drafted position j)
   int32_t x = 0;
   float u = 0.f;
@@ -338,11 +446,11 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
   // the layout is valid, so every access stays in bounds)
   if (s > 0) {
     if (G == 16)
-      combine_pairs<16>(P.part, slot0, s, P.nc, q0, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
+      combine_pairs<16>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_bad, st_arg);
     else if (G == 32)
-      combine_pairs<32>(P.part, slot0, s, P.nc, q0, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
+      combine_pairs<32>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_bad, st_arg);
     else
-      combine_pairs<64>(P.part, slot0, s, P.nc, q0, st_mt, st_md, st_sp, st_sq, st_a, st_bad);
+      combine_pairs<64>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_bad, st_arg);
   }
   __syncthreads();
   if (wave == 0) {
@@ -350,9 +458,9 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
       uint32_t e = 0;
       if (lane < s) {
         if (x < 0 || int64_t(x) >= P.V) e |= DSDE_ERR_TOKEN;
-        if (!(u >= 0.0f && u < 1.0f)) e |= DSDE_ERR_UNIFORM;
+        if (!greedy && !(u >= 0.0f && u < 1.0f)) e |= DSDE_ERR_UNIFORM;
       }
-      if (lane == 0) {
+      if (lane == 0 && !greedy) {
         if (!(T >= kMinTemp && T <= kMaxTemp)) e |= DSDE_ERR_TEMP;
         if (!(ur >= 0.0f && ur < 1.0f)) e |= DSDE_ERR_UNIFORM;
       }
@@ -360,7 +468,7 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
       for (int o = 32; o > 0; o >>= 1) e |= __shfl_xor(e, o);
       err |= e;
     }
-    const float c = kLog2e / T;  // the same expression as the set-up's scale
+    const float c = greedy ? kLog2e : kLog2e / T;  // the same values as the set-up's scale
     const bool active = lane < s && !err;
     bool ok = false, bad = false;
     float my_kld = 0.f;
@@ -374,7 +482,8 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
       // log2 p(x) - log2 q(x); z * c is exact in double
       const double lr = (double(gz.zt) * double(c) - double(st_mt[lane]) - l2sp) -
                         (double(gz.zd) * double(c) - double(st_md[lane]) - l2sq);
-      ok = double(u) < exp2(lr);
+      // greedy: accept iff the drafted token is the target row's argmax
+      ok = greedy ? x == st_arg[lane] : double(u) < exp2(lr);
       if (!bad && P.row_lse) {
         P.row_lse[2 * (first + lane)] = (double(st_mt[lane]) + l2sp) * kLn2;
         P.row_lse[2 * (first + lane) + 1] = (double(st_md[lane]) + l2sq) * kLn2;
@@ -395,7 +504,18 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
       P.accepted[b] = a;
       DrawJob j{};
       j.kind = -1;
-      if (!err) {
+      if (!err && greedy) {
+        j.accepted = a;
+        j.target_row = first + b + a;
+        j.draft_row = -1;
+        if (a < s) {  // the argmax of the first rejected row is known already
+          j.kind = 2;
+          j.token = st_arg[a];
+          tok[a] = st_arg[a];
+        } else {      // the argmax of the bonus row
+          j.kind = 3;
+        }
+      } else if (!err) {
         j.accepted = a;
         j.scale = c;
         j.u = ur;
@@ -422,7 +542,21 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
   // ---- 2. draw-weight totals of every chunk
   const size_t esz = DT == DSDE_BF16 ? 2 : 4;
   const int32_t nc = P.nc;
-  if (job.kind >= 0) {
+  if (job.kind == 3) {
+    const char *trow = (const char *)P.target + size_t(job.target_row) * size_t(P.V) * esz;
+    for (int32_t ch = wave; ch < nc; ch += kSeqWaves) {
+      float zmax;
+      int32_t idx;
+      int bad;
+      bonus_argmax_chunk<DT, VEC>(trow, P.V, ch, &zmax, &idx, &bad);
+      if (lane == 0) {
+        ch_ref[ch] = zmax;
+        ch_arg[ch] = idx;
+        ch_bad[ch] = bad;
+      }
+    }
+    __syncthreads();
+  } else if (job.kind == 0 || job.kind == 1) {
     const char *trow = (const char *)P.target + size_t(job.target_row) * size_t(P.V) * esz;
     if (job.kind == 0) {
       const char *drow = (const char *)P.draft + size_t(job.draft_row) * size_t(P.V) * esz;
@@ -469,8 +603,40 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
       if (e && lane == 0) atomicOr(&P.seq_err[b], e);
     }
   }
-  if (job.kind < 0) {
+  if (job.kind < 0 || job.kind == 2) {  // flagged, or a greedy token already emitted
     if (err && wave == 0 && lane == 0) atomicOr(&P.seq_err[b], err);
+    return;
+  }
+  if (job.kind == 3) {
+    // greedy bonus: the chunk holding the row maximum (the earliest on ties)
+    if (wave == 0) {
+      float best = -INFINITY;
+      int32_t bch = 0x7fffffff;
+      int bad = 0;
+      for (int32_t ch = lane; ch < nc; ch += 64) {
+        bad |= ch_bad[ch];
+        if (bch == 0x7fffffff || ch_ref[ch] > best) {
+          best = ch_ref[ch];
+          bch = ch;
+        }
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) bad |= __shfl_xor(bad, o);
+      const float M = wave_max(best);
+      int32_t cand = bch != 0x7fffffff && best == M ? bch : 0x7fffffff;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) cand = min(cand, __shfl_xor(cand, o));
+      if (bad) {
+        // a NaN or infinite logit in the bonus row: no token is emitted
+        if (lane < width) tok[lane] = P.pad_id;
+        if (lane == 0) {
+          P.accepted[b] = 0;
+          atomicOr(&P.seq_err[b], DSDE_ERR_LOGIT);
+        }
+      } else if (lane == 0) {
+        tok[job.accepted] = ch_arg[cand];
+      }
+    }
     return;
   }
 
@@ -689,7 +855,8 @@ int launch_verify(const VerifyArgs &a) {
   PairChunk *part = (PairChunk *)(ws + L.pair_chunk);
   Gathered *gath = (Gathered *)(ws + L.gathered);
   (void)hipGetLastError();
-  launch_stats_pass(a, work, part, gath);
+  ChunkArg *cargs = (ChunkArg *)(ws + L.chunk_arg);
+  launch_stats_pass(a, work, part, gath, cargs);
   const bool vec = rows_vectorizable(a);
   StepParams P;
   P.target = a.target;
@@ -712,6 +879,7 @@ int launch_verify(const VerifyArgs &a) {
   P.row_lse = a.row_lse;
   P.part = part;
   P.gathered = gath;
+  P.chunk_arg = cargs;
   const SignalArgs S = a.signal ? *a.signal : SignalArgs{};
   if (a.dtype == DSDE_BF16) {
     if (vec)

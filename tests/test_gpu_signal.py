@@ -218,7 +218,7 @@ def clone_state(st):
                          sl_max=st.sl_max.clone())
 
 
-@pytest.mark.parametrize("name", ["tiny", "b64", "b256"])
+@pytest.mark.parametrize("name", ["tiny", "b64", "b256", "greedy"])
 def test_fused_step_equals_the_three_calls(gpu_lib, name):
     cfg = W.CONFIGS[name]
     step = W.make_step(cfg, seed=31, device="cuda")
@@ -242,7 +242,7 @@ def test_fused_step_equals_the_three_calls(gpu_lib, name):
     assert torch.equal(v["seq_err"] | s_["seq_err"] | n_["seq_err"], f["seq_err"])
 
 
-@pytest.mark.parametrize("name", ["b256", "lowacc"])
+@pytest.mark.parametrize("name", ["b256", "lowacc", "b256g"])
 def test_fused_step_parity(gpu_lib, name):
     cfg = W.CONFIGS[name]
     step = W.make_step(cfg, seed=41, device="cuda")

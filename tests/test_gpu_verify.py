@@ -51,7 +51,7 @@ def random_arrays(rng, sls, V, sigma=2.0, noise=1.0):
     return target, draft, tokens, rng.random(N).astype(np.float32), rng.random(B).astype(np.float32)
 
 
-@pytest.mark.parametrize("name", ["tiny", "b64", "b256", "lowacc"])
+@pytest.mark.parametrize("name", ["tiny", "b64", "b256", "lowacc", "greedy", "b256g"])
 def test_workload_parity(gpu_lib, name):
     cfg = W.CONFIGS[name]
     step = W.make_step(cfg, seed=11, device="cuda")
@@ -231,3 +231,49 @@ def test_constructed_ties(gpu_lib):
     step = step_from_arrays(tgt, draft, sls, tokens, [1.0] * B, u_acc, u_res, 1, "fp32")
     _, ref, rep = check_step(gpu_lib, step, "constructed ties")
     assert rep["acc_ties"] >= 24 and rep["cdf_ties"] >= 24, rep
+
+
+@pytest.mark.parametrize("V,dtype", [(5000, "bf16"), (5000, "fp32"), (8200, "bf16"), (600000, "bf16")])
+def test_greedy_ties_and_emissions(gpu_lib, V, dtype):
+    """Greedy verification (T = 0) with repeated maxima inside and across
+    chunks: the argmax is the smallest token id holding the maximum; drafts hit
+    it, miss it, or sit on a later tied maximum."""
+    rng = np.random.default_rng(V % 997 + 3)
+    sls = [3, 2, 4, 0, 1, 5]
+    sl, cu = packed_layout(sls)
+    B = len(sls)
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V, noise=0.8)
+    for r in range(target.shape[0]):
+        m = np.float32(target[r].max() + 2.0)
+        cols = np.sort(rng.choice(V, 3, replace=False))  # three equal maxima, maybe in different chunks
+        target[r, cols] = m
+    for b, s in enumerate(sls):
+        for j in range(s):
+            r = cu[b] + b + j
+            ties = np.nonzero(target[r] == target[r].max())[0]
+            pick = rng.integers(0, 3)
+            tokens[cu[b] + j] = ties[0] if pick == 0 else (ties[-1] if pick == 1 else (ties[0] + 1) % V)
+    temps = np.zeros(B, np.float32)
+    temps[1::3] = 1.0  # a few sampling sequences in between
+    step = step_from_arrays(target, draft, sls, tokens, temps, u_acc, u_res, 5, dtype)
+    got, ref, rep = check_step(gpu_lib, step, f"greedy ties V={V} {dtype}")
+    assert rep["compared"] + rep["acc_ties"] + rep["cdf_ties"] >= B - 1
+
+
+def test_greedy_ignores_uniforms_and_flags_a_bad_bonus_row(gpu_lib):
+    rng = np.random.default_rng(51)
+    sls = [2, 2, 3]
+    V = 3000
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V)
+    sl, cu = packed_layout(sls)
+    for b, s in enumerate(sls):  # every draft is the target argmax: all accepted, bonus sampled
+        for j in range(s):
+            tokens[cu[b] + j] = int(np.argmax(target[cu[b] + b + j]))
+    u_acc[:] = 7.0   # not in [0, 1): unused by greedy sequences
+    u_res[:] = -1.0
+    target[cu[2] + 2 + 3, 11] = np.inf  # sequence 2's bonus row
+    step = step_from_arrays(target, draft, sls, tokens, [0.0, 0.0, 0.0], u_acc, u_res, 3)
+    got, ref, _ = check_step(gpu_lib, step, "greedy: unused uniforms, bad bonus row")
+    assert list(got["seq_err"]) == [0, 0, 4]
+    assert list(got["accepted"][:2]) == [2, 2]
+    assert np.isfinite(got["kld"]).all()

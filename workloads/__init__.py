@@ -18,6 +18,10 @@ are not available here):
           1.0 for odd sequences; W=32.
   lowacc  B=512, SL ~ U{1..16}, V=152064 bf16, draft = 0.5 z + N(0, 3^2) (a weakly
           correlated drafter: acceptance well below 0.4); T=1; W=32; SL_max=16.
+  greedy  b64 with T=0 (greedy verification; drafts are the draft argmax) for even
+          and T=1 for odd sequences.
+  b256g   b256 with T=0 for every sequence (the temperature-0.0 setting of the
+          paper's experiments).
   loop    B=1024, V=128256 bf16, 200 steps; per-sequence sigma follows a reflected
           random walk in [0.2, 4]; SL chosen each step by the controller; W=32,
           empty ring at the start; fresh logits every step.
@@ -44,6 +48,11 @@ CONFIGS = {
     "lowacc": dict(B=512, sl=("uniform", 1, 16), V=152064, dtype="bf16", sigma_z=4.0, zipf=1.05,
                    draft=("weak", 0.5, 3.0), temp=("all", 1.0), W=32, sl_max=16.0, k_max=16,
                    prefill=True),
+    "greedy": dict(B=64, sl=("uniform", 1, 8), V=32000, dtype="bf16", sigma_z=3.0, zipf=1.1,
+                   draft=("noise", 0.3, 3.0), temp=("alternate", 0.0, 1.0), W=16, sl_max=8.0, k_max=8,
+                   prefill=True),
+    "b256g": dict(B=256, sl=("uniform", 1, 8), V=128256, dtype="bf16", sigma_z=4.0, zipf=1.05,
+                  draft=("noise", 0.2, 4.0), temp=("all", 0.0), W=32, sl_max=8.0, k_max=8, prefill=True),
     "loop": dict(B=1024, sl=("uniform", 2, 8), V=128256, dtype="bf16", sigma_z=4.0, zipf=1.05,
                  draft=("walk", 0.2, 4.0), temp=("all", 1.0), W=32, sl_max=8.0, k_max=8, prefill=False,
                  steps=200),
@@ -200,16 +209,19 @@ def make_step(cfg, seed=0, device="cpu", step=0, sl=None, sigma=None, V=None, B=
     draft = y.to(dt)
     del y
 
-    # drafted tokens ~ softmax(draft / T) by Gumbel-max, row by row block
+    # drafted tokens ~ softmax(draft / T) by Gumbel-max, row by row block; at
+    # T = 0 (greedy drafting) the draft row's argmax
     g_k = _gen(device, seed, "tokens", step)
     temp_pos = torch.as_tensor(temp[seq_of_pos], device=device)[:, None]
+    sampled = (temp_pos != 0).to(torch.float32)
+    t_div = torch.where(temp_pos != 0, temp_pos, torch.ones_like(temp_pos))
     toks = torch.empty(N, dtype=torch.int64, device=device)
     for r0 in range(0, N, CH):
         r1 = min(N, r0 + CH)
         u = torch.rand((r1 - r0, V), generator=g_k, device=device, dtype=torch.float32)
         u.clamp_(min=1e-30)
         gumbel = -torch.log(-torch.log(u))
-        toks[r0:r1] = torch.argmax(draft[r0:r1].float() / temp_pos[r0:r1] + gumbel, dim=1)
+        toks[r0:r1] = torch.argmax(draft[r0:r1].float() / t_div[r0:r1] + gumbel * sampled[r0:r1], dim=1)
 
     u_acc = torch.rand(N, generator=_gen(device, seed, "uacc", step), device=device, dtype=torch.float32)
     u_res = torch.rand(B, generator=_gen(device, seed, "ures", step), device=device, dtype=torch.float32)
