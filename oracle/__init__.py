@@ -33,12 +33,12 @@ def _load():
     P = ctypes.c_void_p
     i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
     lib.oracle_verify.argtypes = [P, P, i32, i64, i32, i32, i64, P, P, P, P, P, P, i32,
-                                  P, P, P, P, P, P, P, P, i32]
+                                  P, P, P, P, P, P, P, P, P, i32]
     lib.oracle_verify.restype = i32
     lib.oracle_kld_signal.argtypes = [i32, i64, P, P, P, P, P, P, i32, i32, i32, f64, f64,
                                       P, P, P, P, P, P]
     lib.oracle_kld_signal.restype = i32
-    lib.oracle_next_sl.argtypes = [i32, P, P, P, f64, i32, P, P, P, P]
+    lib.oracle_next_sl.argtypes = [i32, P, P, P, f64, i32, P, P, P, P, P]
     lib.oracle_next_sl.restype = i32
     lib.oracle_calibrate_sl_max.argtypes = [i32, P, i64, P, f64]
     lib.oracle_calibrate_sl_max.restype = f64
@@ -62,7 +62,8 @@ def verify(target, draft, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res,
 
     ``target``: [N+B, V] and ``draft``: [N, V] logits (uint16 bf16 bits or float32).
     Returns a dict of numpy arrays: accepted [B], tokens [B, k_max+1], kld [N] (fp64),
-    lse [N, 2] (fp64), seq_err [B], acc_tie [B], cdf_tie [B], sample_mass [B].
+    lse [N, 2] (fp64), entropy [N] (H(q) in nats, fp64), seq_err [B], acc_tie [B],
+    cdf_tie [B], sample_mass [B].
     """
     lib = _load()
     if target.dtype == np.uint16:
@@ -87,6 +88,7 @@ def verify(target, draft, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res,
         "tokens": np.zeros((B, k_max + 1), np.int32),
         "kld": np.full(max(N, 1), np.nan, np.float64)[:N],
         "lse": np.full((max(N, 1), 2), np.nan, np.float64)[:N],
+        "entropy": np.full(max(N, 1), np.nan, np.float64)[:N],
         "seq_err": np.zeros(B, np.uint32),
         "acc_tie": np.zeros(B, np.int32),
         "cdf_tie": np.zeros(B, np.int32),
@@ -94,7 +96,7 @@ def verify(target, draft, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res,
     }
     ptr = {k: v.ctypes.data_as(ctypes.c_void_p) for k, v in out.items()}
     rc = lib.oracle_verify(t_p, d_p, dtype, V, B, k_max, N, sl_p, cu_p, tok_p, T_p, ua_p, ur_p,
-                           pad_id, ptr["accepted"], ptr["tokens"], ptr["kld"], ptr["lse"],
+                           pad_id, ptr["accepted"], ptr["tokens"], ptr["kld"], ptr["lse"], ptr["entropy"],
                            ptr["seq_err"], ptr["acc_tie"], ptr["cdf_tie"], ptr["sample_mass"],
                            n_threads)
     if rc != 0:
@@ -129,8 +131,9 @@ def kld_signal(sl, cu_sl, kld, hist, head, count, n_short=10, n_long=30, delta=0
     return out
 
 
-def next_sl(sf, wvir, sl_max, sl_min=2.0, sl_hi=8):
-    """SL rule (Eqs. 2, 8) and batch cap (Eqs. 9-11) (see ``oracle_next_sl``)."""
+def next_sl(sf, wvir, sl_max, sl_min=2.0, sl_hi=8, budget=None):
+    """SL rule (Eqs. 2, 8) and batch cap (Eqs. 9-11) (see ``oracle_next_sl``);
+    ``budget`` [B] int32 (optional): tokens each sequence may still emit."""
     lib = _load()
     sf_a, sf_p = _c(sf, np.float64)
     wv_a, wv_p = _c(wvir, np.float64)
@@ -141,7 +144,10 @@ def next_sl(sf, wvir, sl_max, sl_min=2.0, sl_hi=8):
     nxt = np.zeros(B, np.int32)
     err = np.zeros(B, np.uint32)
     P = lambda a: a.ctypes.data_as(ctypes.c_void_p)
-    rc = lib.oracle_next_sl(B, sf_p, wv_p, mx_p, sl_min, sl_hi, P(hat), P(cap), P(nxt), P(err))
+    bud_p = None
+    if budget is not None:
+        bud_a, bud_p = _c(budget, np.int32)
+    rc = lib.oracle_next_sl(B, sf_p, wv_p, mx_p, sl_min, sl_hi, bud_p, P(hat), P(cap), P(nxt), P(err))
     if rc != 0:
         raise ValueError("oracle_next_sl rejected its arguments")
     return {"sl_hat": hat, "sl_cap": float(cap[0]), "sl_next": nxt, "seq_err": err}

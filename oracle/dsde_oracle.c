@@ -28,6 +28,13 @@
  *                        of the predicted lengths).
  *   oracle_calibrate_sl_max -- Eq. 1 (Sec. 3.1.1).
  *
+ * Also: the entropy H(q) of every drafted position's tempered draft
+ * distribution (the draft-entropy signal the paper compares against, Sec. 4.2
+ * and Table 2), and a per-sequence token budget that bounds the next
+ * speculation length (the clamp under remaining max_tokens and context
+ * capacity of the policy interface, Sec. 3.2): a step emits up to SL + 1
+ * tokens, so SL_next <= max(budget - 1, 0).
+ *
  * Greedy verification (the temperature-0.0 setting of the experiments, Sec. 4.2
  * and Table 3(a)): a sequence with T_b = 0 accepts a drafted token iff it is
  * the argmax of its target row (the smallest token id among equal maxima) and
@@ -133,6 +140,7 @@ typedef struct {
   /* outputs */
   int32_t *accepted, *tokens;
   double *kld, *lse; /* lse: [N, 2] (p, q), may be NULL */
+  double *entropy;   /* [N] H(q) in nats, may be NULL */
   uint32_t *seq_err;
   int32_t *acc_tie, *cdf_tie;
   double *sample_mass; /* [B]: Z of the draw (probability mass), may be NULL */
@@ -197,6 +205,16 @@ static void verify_sequence(const verify_job *J, int32_t b) {
       if (p > 0.0) kl += p * (lp - lq);
     }
     J->kld[first + j] = kl > 0.0 ? kl : 0.0;
+    if (J->entropy) {
+      /* H(q) = -sum_v q_v log q_v of the same tempered draft distribution */
+      double h = 0.0;
+      for (int64_t v = 0; v < V; ++v) {
+        double lq = logit(J->draft, J->dtype, V, dr, v) / T - lse_q[j];
+        double q = exp(lq);
+        if (q > 0.0) h -= q * lq;
+      }
+      J->entropy[first + j] = h;
+    }
     if (J->lse) {
       J->lse[2 * (first + j)] = lse_p[j];
       J->lse[2 * (first + j) + 1] = lse_q[j];
@@ -314,6 +332,8 @@ static void verify_sequence(const verify_job *J, int32_t b) {
 fail:
   J->seq_err[b] = err;
   for (int32_t j = 0; j < SL; ++j) J->kld[first + j] = NAN;
+  if (J->entropy)
+    for (int32_t j = 0; j < SL; ++j) J->entropy[first + j] = NAN;
 }
 
 static void *verify_worker(void *arg) {
@@ -337,14 +357,15 @@ static int layout_valid(int32_t B, int64_t N, int32_t k_max, const int32_t *sl, 
 int oracle_verify(const void *target, const void *draft, int32_t dtype, int64_t V, int32_t B, int32_t k_max,
                   int64_t N, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
                   const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
-                  int32_t *accepted, int32_t *tokens, double *kld, double *lse, uint32_t *seq_err,
-                  int32_t *acc_tie, int32_t *cdf_tie, double *sample_mass, int32_t n_threads) {
+                  int32_t *accepted, int32_t *tokens, double *kld, double *lse, double *entropy,
+                  uint32_t *seq_err, int32_t *acc_tie, int32_t *cdf_tie, double *sample_mass,
+                  int32_t n_threads) {
   if (B < 1 || V < 1 || k_max < 0 || N < 0 || (dtype != 0 && dtype != 1)) return 1;
   if (n_threads < 1) n_threads = 1;
   if (n_threads > 256) n_threads = 256;
   verify_job base = {target, draft, dtype, V, N, B, k_max, sl, cu_sl, draft_tokens, temperature, u_acc,
                      u_res, pad_id, layout_valid(B, N, k_max, sl, cu_sl), accepted, tokens, kld, lse,
-                     seq_err, acc_tie, cdf_tie, sample_mass, n_threads, 0};
+                     entropy, seq_err, acc_tie, cdf_tie, sample_mass, n_threads, 0};
   verify_job jobs[256];
   pthread_t th[256];
   for (int t = 0; t < n_threads; ++t) {
@@ -465,7 +486,8 @@ static int32_t round_clamp(double x, int32_t lo, int32_t hi) {
 }
 
 int oracle_next_sl(int32_t B, const double *sf, const double *wvir, const double *sl_max, double sl_min,
-                   int32_t sl_hi, double *sl_hat, double *sl_cap, int32_t *sl_next, uint32_t *seq_err) {
+                   int32_t sl_hi, const int32_t *budget, double *sl_hat, double *sl_cap, int32_t *sl_next,
+                   uint32_t *seq_err) {
   if (B < 1 || !isfinite(sl_min) || ceil(sl_min) > (double)sl_hi) return 1;
   const int32_t lo = (int32_t)ceil(sl_min);
   double sum = 0.0;
@@ -491,6 +513,11 @@ int oracle_next_sl(int32_t B, const double *sf, const double *wvir, const double
     double x = sl_hat[b] < cap ? sl_hat[b] : cap;
     sl_next[b] = round_clamp(x, lo, sl_hi);
   }
+  if (budget) /* the step after this one may emit at most budget[b] tokens */
+    for (int32_t b = 0; b < B; ++b) {
+      int32_t room = budget[b] - 1 > 0 ? budget[b] - 1 : 0;
+      if (sl_next[b] > room) sl_next[b] = room;
+    }
   return 0;
 }
 

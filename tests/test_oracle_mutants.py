@@ -38,6 +38,9 @@ MUTANTS = {
     "greedy_tie_takes_last": ("    if (z > m) {\n      m = z;\n      best = v;", "    if (z >= m) {\n      m = z;\n      best = v;"),
     "greedy_emits_next_row": ("tok[a] = (int32_t)row_argmax(J->target, J->dtype, V, trow0 + a);",
                               "tok[a] = (int32_t)row_argmax(J->target, J->dtype, V, trow0 + a + (a < SL));"),
+    "entropy_sign": ("if (q > 0.0) h -= q * lq;", "if (q > 0.0) h += q * lq;"),
+    "budget_off_by_one": ("int32_t room = budget[b] - 1 > 0 ? budget[b] - 1 : 0;",
+                          "int32_t room = budget[b] > 0 ? budget[b] : 0;"),
     "greedy_kld_at_zero_scale": ("const double T = greedy ? 1.0 : (double)J->temperature[b];",
                                  "const double T = greedy ? 2.0 : (double)J->temperature[b];"),
 }

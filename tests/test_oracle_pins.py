@@ -531,3 +531,62 @@ def test_greedy_kld_is_taken_at_unit_temperature_and_uniforms_are_unused(orc):
     unit = orc.verify(**dict(kw, temperature=np.ones(2, np.float32),
                              u_acc=np.zeros(5, np.float32), u_res=np.zeros(2, np.float32)))
     np.testing.assert_array_equal(g["kld"], unit["kld"])
+
+
+# ---------------------------------------------------------------------------
+# draft entropy H(q) (the comparison signal of Sec. 4.2, Table 2)
+# ---------------------------------------------------------------------------
+
+def test_draft_entropy_closed_forms(orc):
+    V = 64
+    sls = [3, 2]
+    rng = np.random.default_rng(61)
+    kw = _random_batch(rng, sls, V, T=1.0)
+    kw["draft"][0] = 0.0                         # uniform: ln V
+    kw["draft"][1] = 0.0
+    kw["draft"][1, 5] = 200.0                    # one-hot: 0
+    kw["draft"][2, :2] = [np.log(3.0), 0.0]      # two tokens with q = 3/4, 1/4: the binary entropy
+    kw["draft"][2, 2:] = -1e4
+    out = orc.verify(**kw)
+    np.testing.assert_allclose(out["entropy"][0], np.log(V), rtol=1e-14)
+    assert 0.0 <= out["entropy"][1] < 1e-80
+    p3 = 1.0 / (1.0 + np.exp(-np.float64(np.float32(np.log(3.0)))))  # q = (3/4, 1/4) up to fp32 rounding of ln 3
+    np.testing.assert_allclose(out["entropy"][2], -(p3 * np.log(p3) + (1 - p3) * np.log(1 - p3)), rtol=1e-12)
+    for n in range(3, 5):  # random rows: the textbook definition
+        q = softmax(kw["draft"][n].astype(np.float64))
+        np.testing.assert_allclose(out["entropy"][n], entropy(q), rtol=1e-12)
+
+
+def test_draft_entropy_is_taken_on_the_tempered_distribution(orc):
+    rng = np.random.default_rng(62)
+    kw = _random_batch(rng, [2, 2], 30, T=1.0)
+    kw["temperature"] = np.array([0.5, 2.0], np.float32)
+    out = orc.verify(**kw)
+    cu = kw["cu_sl"]
+    for b, T in enumerate([0.5, 2.0]):
+        for j in range(2):
+            q = softmax(kw["draft"][cu[b] + j].astype(np.float64) / T)
+            np.testing.assert_allclose(out["entropy"][cu[b] + j], entropy(q), rtol=1e-12)
+    g = orc.verify(**dict(kw, temperature=np.zeros(2, np.float32)))  # greedy: at T = 1
+    for n in range(4):
+        np.testing.assert_allclose(g["entropy"][n], entropy(softmax(kw["draft"][n].astype(np.float64))),
+                                   rtol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# token budget of the policy interface (Sec. 3.2)
+# ---------------------------------------------------------------------------
+
+def test_budget_bounds_the_next_length(orc):
+    rng = np.random.default_rng(63)
+    B = 12
+    sf = rng.uniform(0.0, 0.3, B)
+    wv = rng.uniform(0.0, 2.0, B)
+    mx = np.full(B, 8.0)
+    free = orc.next_sl(sf, wv, mx, 2.0, 8)
+    same = orc.next_sl(sf, wv, mx, 2.0, 8, budget=np.full(B, 10 ** 6, np.int32))
+    assert np.array_equal(free["sl_next"], same["sl_next"])
+    budget = np.array([0, 1, 2, 3, 4, 5, 6, 7, 8, 9, -3, 100], np.int32)
+    got = orc.next_sl(sf, wv, mx, 2.0, 8, budget=budget)
+    assert np.array_equal(got["sl_next"], np.minimum(free["sl_next"], np.maximum(budget - 1, 0)))
+    assert got["sl_cap"] == free["sl_cap"]  # the cap is taken before the budget
