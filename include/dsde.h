@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define DSDE_ABI_VERSION 1
+#define DSDE_ABI_VERSION 2
 
 /* status codes */
 #define DSDE_OK 0
@@ -121,6 +121,9 @@ size_t dsde_verify_workspace_bytes(int32_t B, int64_t N, int64_t V, int32_t k_ma
  *   seq_err [B]             uint32      DSDE_ERR_* bits per sequence (0 when fine)
  *   row_lse [N, 2]          double      optional (may be NULL): natural-log normalisers
  *                                       log sum_v exp(z_v / T_b) of the target and draft rows
+ *   draft_entropy [N]       float       optional (may be NULL): H(q) = -sum_v q_v ln q_v of
+ *                                       each drafted position's draft distribution (nats),
+ *                                       the draft-entropy signal of Sec. 4.2 / Table 2
  * The draw walks token ids in ascending order and returns the smallest id whose
  * cumulative weight exceeds u_res[b] times the total weight.  Acceptance is
  * evaluated as u < p(x)/q(x) in double precision.
@@ -134,8 +137,8 @@ int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t
                     int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl,
                     const int32_t *draft_tokens, const float *temperature, const float *u_acc,
                     const float *u_res, int32_t pad_id, int32_t *accepted, int32_t *tokens, float *kld,
-                    uint32_t *seq_err, double *row_lse, void *workspace, size_t workspace_bytes,
-                    void *stream);
+                    uint32_t *seq_err, double *row_lse, float *draft_entropy, void *workspace,
+                    size_t workspace_bytes, void *stream);
 
 /*
  * KLD stability signal (Sec. 3.1.2, Eqs. 3-7).
@@ -178,14 +181,22 @@ int32_t dsde_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *
  * DSDE_ERR_SIGNAL, sl_hat = NaN and sl_next = ceil(sl_min); with no valid
  * sequence SL_cap is NaN.
  *
+ * Then the per-sequence token budget of the policy interface (Sec. 3.2: the
+ * length is clamped under the remaining max_tokens and context capacity): a
+ * step emits up to SL + 1 tokens, so sl_next[b] = min(sl_next[b],
+ * max(budget[b] - 1, 0)).  The budget wins over sl_min; the cap is taken
+ * before the budget.
+ *
  *   sf [B], wvir [B], sl_max [B]   float
  *   sl_min                          finite; ceil(sl_min) <= sl_hi (paper: SL_min = 2)
  *   sl_hi                           upper bound of the next step's SL (its k_max)
+ *   budget [B]                      int32, optional (may be NULL): tokens each sequence
+ *                                   may still emit
  * Outputs: sl_hat [B] float, sl_cap [1] float, sl_next [B] int32, seq_err [B] uint32.
  */
 int32_t dsde_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max, float sl_min,
-                     int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
-                     void *stream);
+                     int32_t sl_hi, const int32_t *budget, float *sl_hat, float *sl_cap, int32_t *sl_next,
+                     uint32_t *seq_err, void *stream);
 
 /*
  * The whole step fused: dsde_verify, then dsde_kld_signal on the KLD it
@@ -199,11 +210,36 @@ int32_t dsde_next_sl(int32_t B, const float *sf, const float *wvir, const float 
 int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
                   int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
                   const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
-                  int32_t *accepted, int32_t *tokens, float *kld, double *row_lse, float *hist, int32_t *head,
-                  int32_t *count, int32_t W, int32_t n_short, int32_t n_long, float delta, float eps,
-                  float *mu_last, float *var_short, float *var_long, float *wvir, float *sf, const float *sl_max,
-                  float sl_min, int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
-                  void *workspace, size_t workspace_bytes, void *stream);
+                  int32_t *accepted, int32_t *tokens, float *kld, double *row_lse, float *draft_entropy,
+                  float *hist, int32_t *head, int32_t *count, int32_t W, int32_t n_short, int32_t n_long,
+                  float delta, float eps, float *mu_last, float *var_short, float *var_long, float *wvir, float *sf,
+                  const float *sl_max, float sl_min, int32_t sl_hi, const int32_t *budget, float *sl_hat,
+                  float *sl_cap, int32_t *sl_next, uint32_t *seq_err, void *workspace, size_t workspace_bytes,
+                  void *stream);
+
+/*
+ * SL_max calibration (Sec. 3.1.1, Eq. 1):
+ *   SL_max = SL_A,max * (1 + mu_KLD,pre / (KLD_pre,max + eps))
+ * over a few preliminary steps: SL_A,max the largest number of drafts accepted
+ * in one step, mu_KLD,pre the mean of every per-token KLD seen, KLD_pre,max
+ * the largest one.
+ *
+ * dsde_calibration_update folds one verification step (its sl, cu_sl,
+ * accepted, kld and seq_err, as dsde_verify produced them) into running
+ * per-sequence statistics; sequences with error bits are skipped, and an
+ * invalid layout skips the whole step.  The caller zeroes the statistics
+ * before the first step:
+ *   a_max [B] int32, kld_sum [B] double, kld_count [B] int64, kld_max [B] float  (in/out)
+ * dsde_calibrate_sl_max evaluates Eq. 1 into sl_max [B] (float): per sequence
+ * (pooled = 0) or, pooled = 1, from the statistics pooled over the batch (the
+ * same value for every sequence).  A sequence without KLD values has mean 0.
+ *   eps >= 0 (paper: 1e-6)
+ */
+int32_t dsde_calibration_update(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu_sl,
+                                const int32_t *accepted, const float *kld, const uint32_t *seq_err, int32_t *a_max,
+                                double *kld_sum, int64_t *kld_count, float *kld_max, void *stream);
+int32_t dsde_calibrate_sl_max(int32_t B, const int32_t *a_max, const double *kld_sum, const int64_t *kld_count,
+                              const float *kld_max, float eps, int32_t pooled, float *sl_max, void *stream);
 
 /*
  * Measurement utility, not part of the method: reads `bytes` bytes of device

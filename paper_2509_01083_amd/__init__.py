@@ -19,7 +19,8 @@ FP32, BF16 = 0, 1
 ERR_LAYOUT, ERR_TOKEN, ERR_LOGIT, ERR_TEMP, ERR_UNIFORM, ERR_SIGNAL, ERR_STATE = 1, 2, 4, 8, 16, 32, 64
 MAX_K = 63
 EXPORTS = ("dsde_abi_version", "dsde_status_string", "dsde_verify_workspace_bytes", "dsde_verify",
-           "dsde_step", "dsde_kld_signal", "dsde_next_sl", "dsde_set_profile_events", "dsde_stream_read")
+           "dsde_step", "dsde_kld_signal", "dsde_next_sl", "dsde_calibration_update", "dsde_calibrate_sl_max",
+           "dsde_set_profile_events", "dsde_stream_read")
 
 _lib = None
 
@@ -45,15 +46,19 @@ def load(path: str = LIB_PATH):
     lib.dsde_verify_workspace_bytes.restype = sz
     lib.dsde_verify_workspace_bytes.argtypes = [i32, i64, i64, i32]
     lib.dsde_verify.restype = i32
-    lib.dsde_verify.argtypes = [P, P, i32, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P, P, P, sz, P]
+    lib.dsde_verify.argtypes = [P, P, i32, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P, P, P, P, sz, P]
     lib.dsde_step.restype = i32
-    lib.dsde_step.argtypes = [P, P, i32, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P,
+    lib.dsde_step.argtypes = [P, P, i32, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P, P,
                               P, P, P, i32, i32, i32, f32, f32, P, P, P, P, P,
-                              P, f32, i32, P, P, P, P, P, sz, P]
+                              P, f32, i32, P, P, P, P, P, P, sz, P]
     lib.dsde_kld_signal.restype = i32
     lib.dsde_kld_signal.argtypes = [i32, i64, P, P, P, P, P, P, i32, i32, i32, f32, f32, P, P, P, P, P, P, P]
     lib.dsde_next_sl.restype = i32
-    lib.dsde_next_sl.argtypes = [i32, P, P, P, f32, i32, P, P, P, P, P]
+    lib.dsde_next_sl.argtypes = [i32, P, P, P, f32, i32, P, P, P, P, P, P]
+    lib.dsde_calibration_update.restype = i32
+    lib.dsde_calibration_update.argtypes = [i32, i64, P, P, P, P, P, P, P, P, P, P]
+    lib.dsde_calibrate_sl_max.restype = i32
+    lib.dsde_calibrate_sl_max.argtypes = [i32, P, P, P, P, f32, i32, P, P]
     lib.dsde_set_profile_events.restype = i32
     lib.dsde_set_profile_events.argtypes = [P, P]
     lib.dsde_stream_read.restype = i32
@@ -98,9 +103,10 @@ def new_workspace(B, N, V, k_max, device="cuda"):
 
 
 def verify(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, pad_id=-1,
-           out=None, workspace=None, row_lse=None, stream=None):
-    """``dsde_verify`` on torch tensors.  Returns (accepted, tokens, kld, seq_err);
-    pass ``out`` (a dict with those keys) to reuse output buffers."""
+           out=None, workspace=None, row_lse=None, draft_entropy=False, stream=None):
+    """``dsde_verify`` on torch tensors.  Returns a dict with accepted, tokens, kld,
+    seq_err (and draft_entropy when asked for); pass ``out`` (a dict with those
+    keys) to reuse output buffers."""
     lib = load()
     dt = _logits_dtype(target)
     V = int(target.shape[1])
@@ -116,6 +122,9 @@ def verify(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_
                "tokens": torch.empty((B, k_max + 1), dtype=torch.int32, device=dev),
                "kld": torch.empty(max(N, 1), dtype=torch.float32, device=dev)[:N],
                "seq_err": torch.empty(B, dtype=torch.int32, device=dev)}
+    if draft_entropy and "draft_entropy" not in out:
+        out["draft_entropy"] = torch.empty(max(N, 1), dtype=torch.float32, device=dev)[:N]
+    ent = out.get("draft_entropy") if draft_entropy else None
     if workspace is None:
         workspace = new_workspace(B, N, V, k_max, device=dev)
     rc = lib.dsde_verify(
@@ -130,6 +139,7 @@ def verify(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_
         _ptr(out["kld"], torch.float32, N, "kld") if N > 0 else None,
         _ptr(out["seq_err"], None, B, "seq_err"),
         _ptr(row_lse, torch.float64, 2 * N, "row_lse") if row_lse is not None else None,
+        _ptr(ent, torch.float32, N, "draft_entropy") if ent is not None and N > 0 else None,
         _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(), _stream(stream))
     _check(rc)
     return out
@@ -145,10 +155,11 @@ def _logits_dtype(target):
 
 def step(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, hist, head, count,
          sl_max, n_short=10, n_long=30, delta=0.85, eps=1e-6, sl_min=2.0, sl_hi=None, pad_id=-1,
-         out=None, workspace=None, row_lse=None, stream=None):
+         out=None, workspace=None, row_lse=None, draft_entropy=False, budget=None, stream=None):
     """``dsde_step``: verify + signal update + SL rule in one call.  hist/head/count are
     updated in place; returns a dict of every output (accepted, tokens, kld, mu_last,
-    var_short, var_long, wvir, sf, sl_hat, sl_cap, sl_next, seq_err)."""
+    var_short, var_long, wvir, sf, sl_hat, sl_cap, sl_next, seq_err, and draft_entropy
+    when asked for).  ``budget`` [B] int32: tokens each sequence may still emit."""
     lib = load()
     dt = _logits_dtype(target)
     V = int(target.shape[1])
@@ -168,6 +179,9 @@ def step(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_ma
                "sl_next": torch.empty(B, dtype=torch.int32, device=dev)}
         for k in ("mu_last", "var_short", "var_long", "wvir", "sf", "sl_hat"):
             out[k] = torch.empty(B, dtype=torch.float32, device=dev)
+    if draft_entropy and "draft_entropy" not in out:
+        out["draft_entropy"] = torch.empty(max(N, 1), dtype=torch.float32, device=dev)[:N]
+    ent = out.get("draft_entropy") if draft_entropy else None
     if workspace is None:
         workspace = new_workspace(B, N, V, k_max, device=dev)
     f32 = torch.float32
@@ -180,11 +194,13 @@ def step(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_ma
         _ptr(out["accepted"], torch.int32, B), _ptr(out["tokens"], torch.int32, B * (k_max + 1)),
         _ptr(out["kld"], f32, N) if N > 0 else None,
         _ptr(row_lse, torch.float64, 2 * N, "row_lse") if row_lse is not None else None,
+        _ptr(ent, f32, N, "draft_entropy") if ent is not None and N > 0 else None,
         _ptr(hist, f32, B * W, "hist"), _ptr(head, torch.int32, B, "head"), _ptr(count, torch.int32, B, "count"),
         W, n_short, n_long, float(delta), float(eps),
         _ptr(out["mu_last"], f32, B), _ptr(out["var_short"], f32, B), _ptr(out["var_long"], f32, B),
         _ptr(out["wvir"], f32, B), _ptr(out["sf"], f32, B), _ptr(sl_max, f32, B, "sl_max"), float(sl_min),
-        int(sl_hi), _ptr(out["sl_hat"], f32, B), _ptr(out["sl_cap"], f32, 1), _ptr(out["sl_next"], torch.int32, B),
+        int(sl_hi), _ptr(budget, torch.int32, B, "budget") if budget is not None else None,
+        _ptr(out["sl_hat"], f32, B), _ptr(out["sl_cap"], f32, 1), _ptr(out["sl_next"], torch.int32, B),
         _ptr(out["seq_err"], None, B), _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
         _stream(stream))
     _check(rc)
@@ -214,8 +230,9 @@ def kld_signal(sl, cu_sl, kld, hist, head, count, n_short=10, n_long=30, delta=0
     return out
 
 
-def next_sl(sf, wvir, sl_max, sl_min=2.0, sl_hi=8, out=None, stream=None):
-    """``dsde_next_sl``: SL rule with the batch cap; returns sl_hat, sl_cap, sl_next, seq_err."""
+def next_sl(sf, wvir, sl_max, sl_min=2.0, sl_hi=8, budget=None, out=None, stream=None):
+    """``dsde_next_sl``: SL rule with the batch cap (and the optional per-sequence
+    token budget); returns sl_hat, sl_cap, sl_next, seq_err."""
     lib = load()
     B = int(sf.shape[0])
     dev = sf.device
@@ -226,9 +243,44 @@ def next_sl(sf, wvir, sl_max, sl_min=2.0, sl_hi=8, out=None, stream=None):
                "seq_err": torch.empty(B, dtype=torch.int32, device=dev)}
     rc = lib.dsde_next_sl(B, _ptr(sf, torch.float32, B, "sf"), _ptr(wvir, torch.float32, B, "wvir"),
                           _ptr(sl_max, torch.float32, B, "sl_max"), float(sl_min), int(sl_hi),
+                          _ptr(budget, torch.int32, B, "budget") if budget is not None else None,
                           _ptr(out["sl_hat"], torch.float32, B), _ptr(out["sl_cap"], torch.float32, 1),
                           _ptr(out["sl_next"], torch.int32, B), _ptr(out["seq_err"], None, B), _stream(stream))
     _check(rc)
+    return out
+
+
+def new_calibration_state(B, device="cuda"):
+    """Zeroed running statistics of the SL_max calibration (Eq. 1)."""
+    return {"a_max": torch.zeros(B, dtype=torch.int32, device=device),
+            "kld_sum": torch.zeros(B, dtype=torch.float64, device=device),
+            "kld_count": torch.zeros(B, dtype=torch.int64, device=device),
+            "kld_max": torch.zeros(B, dtype=torch.float32, device=device)}
+
+
+def calibration_update(sl, cu_sl, accepted, kld, seq_err, state, stream=None):
+    """``dsde_calibration_update``: folds one verification step into ``state``."""
+    lib = load()
+    B = int(sl.shape[0])
+    N = int(kld.shape[0])
+    _check(lib.dsde_calibration_update(
+        B, N, _ptr(sl, torch.int32, B, "sl"), _ptr(cu_sl, torch.int32, B + 1, "cu_sl"),
+        _ptr(accepted, torch.int32, B, "accepted"), _ptr(kld, torch.float32, N, "kld") if N > 0 else None,
+        _ptr(seq_err, None, B, "seq_err"), _ptr(state["a_max"], torch.int32, B),
+        _ptr(state["kld_sum"], torch.float64, B), _ptr(state["kld_count"], torch.int64, B),
+        _ptr(state["kld_max"], torch.float32, B), _stream(stream)))
+
+
+def calibrate_sl_max(state, eps=1e-6, pooled=False, out=None, stream=None):
+    """``dsde_calibrate_sl_max``: Eq. 1 per sequence, or pooled over the batch."""
+    lib = load()
+    B = int(state["a_max"].shape[0])
+    if out is None:
+        out = torch.empty(B, dtype=torch.float32, device=state["a_max"].device)
+    _check(lib.dsde_calibrate_sl_max(
+        B, _ptr(state["a_max"], torch.int32, B), _ptr(state["kld_sum"], torch.float64, B),
+        _ptr(state["kld_count"], torch.int64, B), _ptr(state["kld_max"], torch.float32, B), float(eps),
+        1 if pooled else 0, _ptr(out, torch.float32, B), _stream(stream)))
     return out
 
 

@@ -49,8 +49,8 @@ int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t
                     int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl,
                     const int32_t *draft_tokens, const float *temperature, const float *u_acc,
                     const float *u_res, int32_t pad_id, int32_t *accepted, int32_t *tokens, float *kld,
-                    uint32_t *seq_err, double *row_lse, void *workspace, size_t workspace_bytes,
-                    void *stream) {
+                    uint32_t *seq_err, double *row_lse, float *draft_entropy, void *workspace,
+                    size_t workspace_bytes, void *stream) {
   if (dtype != DSDE_FP32 && dtype != DSDE_BF16) return DSDE_INVALID_ARG;
   if (!verify_sizes_ok(B, N, V, k_max)) return DSDE_INVALID_ARG;
   if (!target_logits || !sl || !cu_sl || !temperature || !u_res || !accepted || !tokens || !seq_err ||
@@ -79,6 +79,7 @@ int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t
   a.kld = kld;
   a.seq_err = seq_err;
   a.row_lse = row_lse;
+  a.draft_entropy = draft_entropy;
   a.workspace = workspace;
   a.stream = static_cast<hipStream_t>(stream);
   a.prof_start = g_prof_start;
@@ -90,11 +91,12 @@ int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t
 int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
                   int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
                   const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
-                  int32_t *accepted, int32_t *tokens, float *kld, double *row_lse, float *hist, int32_t *head,
-                  int32_t *count, int32_t W, int32_t n_short, int32_t n_long, float delta, float eps,
-                  float *mu_last, float *var_short, float *var_long, float *wvir, float *sf, const float *sl_max,
-                  float sl_min, int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
-                  void *workspace, size_t workspace_bytes, void *stream) {
+                  int32_t *accepted, int32_t *tokens, float *kld, double *row_lse, float *draft_entropy,
+                  float *hist, int32_t *head, int32_t *count, int32_t W, int32_t n_short, int32_t n_long,
+                  float delta, float eps, float *mu_last, float *var_short, float *var_long, float *wvir, float *sf,
+                  const float *sl_max, float sl_min, int32_t sl_hi, const int32_t *budget, float *sl_hat,
+                  float *sl_cap, int32_t *sl_next, uint32_t *seq_err, void *workspace, size_t workspace_bytes,
+                  void *stream) {
   if (dtype != DSDE_FP32 && dtype != DSDE_BF16) return DSDE_INVALID_ARG;
   if (!verify_sizes_ok(B, N, V, k_max)) return DSDE_INVALID_ARG;
   if (!target_logits || !sl || !cu_sl || !temperature || !u_res || !accepted || !tokens || !seq_err ||
@@ -125,6 +127,7 @@ int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t d
   sg.sl_max = sl_max;
   sg.sl_min = sl_min;
   sg.sl_hi = sl_hi;
+  sg.budget = budget;
   sg.sl_hat = sl_hat;
   sg.sl_cap = sl_cap;
   sg.sl_next = sl_next;
@@ -148,6 +151,7 @@ int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t d
   a.kld = kld;
   a.seq_err = seq_err;
   a.row_lse = row_lse;
+  a.draft_entropy = draft_entropy;
   a.workspace = workspace;
   a.stream = static_cast<hipStream_t>(stream);
   a.prof_start = g_prof_start;
@@ -171,12 +175,31 @@ int32_t dsde_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *
 }
 
 int32_t dsde_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max, float sl_min,
-                     int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
-                     void *stream) {
+                     int32_t sl_hi, const int32_t *budget, float *sl_hat, float *sl_cap, int32_t *sl_next,
+                     uint32_t *seq_err, void *stream) {
   if (B < 1 || !isfinite(sl_min) || ceilf(sl_min) > float(sl_hi)) return DSDE_INVALID_ARG;
   if (!sf || !wvir || !sl_max || !sl_hat || !sl_cap || !sl_next || !seq_err) return DSDE_INVALID_ARG;
-  return dsde::launch_next_sl(B, sf, wvir, sl_max, sl_min, sl_hi, sl_hat, sl_cap, sl_next, seq_err, false,
+  return dsde::launch_next_sl(B, sf, wvir, sl_max, sl_min, sl_hi, budget, sl_hat, sl_cap, sl_next, seq_err, false,
                               static_cast<hipStream_t>(stream));
+}
+
+int32_t dsde_calibration_update(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu_sl,
+                                const int32_t *accepted, const float *kld, const uint32_t *seq_err, int32_t *a_max,
+                                double *kld_sum, int64_t *kld_count, float *kld_max, void *stream) {
+  if (B < 1 || N < 0) return DSDE_INVALID_ARG;
+  if (!sl || !cu_sl || !accepted || !seq_err || !a_max || !kld_sum || !kld_count || !kld_max)
+    return DSDE_INVALID_ARG;
+  if (N > 0 && !kld) return DSDE_INVALID_ARG;
+  return dsde::launch_calibration_update(B, N, sl, cu_sl, accepted, kld, seq_err, a_max, kld_sum, kld_count, kld_max,
+                                         static_cast<hipStream_t>(stream));
+}
+
+int32_t dsde_calibrate_sl_max(int32_t B, const int32_t *a_max, const double *kld_sum, const int64_t *kld_count,
+                              const float *kld_max, float eps, int32_t pooled, float *sl_max, void *stream) {
+  if (B < 1 || !(eps >= 0.0f) || !isfinite(eps) || (pooled != 0 && pooled != 1)) return DSDE_INVALID_ARG;
+  if (!a_max || !kld_sum || !kld_count || !kld_max || !sl_max) return DSDE_INVALID_ARG;
+  return dsde::launch_calibrate_sl_max(B, a_max, kld_sum, kld_count, kld_max, eps, pooled != 0, sl_max,
+                                       static_cast<hipStream_t>(stream));
 }
 
 int32_t dsde_set_profile_events(void *start, void *stop) {

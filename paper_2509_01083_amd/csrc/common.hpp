@@ -37,10 +37,11 @@ struct WorkItem {
 // Row statistics of one chunk of one drafted row pair, relative to the
 // chunk's reference shifts mt, md (log2 domain):
 //   sp = sum 2^(z_t c - mt),  sq = sum 2^(z_d c - md),
-//   a  = sum 2^(z_t c - mt) * ((z_t c - mt) - (z_d c - md)).
+//   a  = sum 2^(z_t c - mt) * ((z_t c - mt) - (z_d c - md)),
+//   h  = sum 2^(z_d c - md) * (z_d c - md).
 struct alignas(16) PairChunk {
   float mt, md;
-  double sp, sq, a;
+  double sp, sq, a, h;
 };
 
 // Greedy pairs: the target row's largest logit in a chunk (raw, unscaled) and
@@ -98,6 +99,7 @@ struct SignalArgs {
   const float *sl_max;
   float sl_min;
   int32_t sl_hi;
+  const int32_t *budget;  // may be null
   float *sl_hat, *sl_cap;
   int32_t *sl_next;
 };
@@ -116,6 +118,7 @@ struct VerifyArgs {
   float *kld;
   uint32_t *seq_err;
   double *row_lse;
+  float *draft_entropy;
   void *workspace;
   hipStream_t stream;
   hipEvent_t prof_start, prof_stop;
@@ -131,9 +134,14 @@ int launch_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu
                       float *hist, int32_t *head, int32_t *count, int32_t W, int32_t n_short, int32_t n_long,
                       float delta, float eps, float *mu_last, float *var_short, float *var_long, float *wvir,
                       float *sf, uint32_t *seq_err, hipStream_t stream);
+int launch_calibration_update(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu_sl, const int32_t *accepted,
+                              const float *kld, const uint32_t *seq_err, int32_t *a_max, double *kld_sum,
+                              int64_t *kld_count, float *kld_max, hipStream_t stream);
+int launch_calibrate_sl_max(int32_t B, const int32_t *a_max, const double *kld_sum, const int64_t *kld_count,
+                            const float *kld_max, float eps, bool pooled, float *sl_max, hipStream_t stream);
 int launch_stream_read(const void *buf, int64_t bytes, uint32_t *out, hipStream_t stream);
 int launch_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max, float sl_min,
-                   int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err, bool or_err,
-                   hipStream_t stream);
+                   int32_t sl_hi, const int32_t *budget, float *sl_hat, float *sl_cap, int32_t *sl_next,
+                   uint32_t *seq_err, bool or_err, hipStream_t stream);
 
 }  // namespace dsde

@@ -127,20 +127,24 @@ __device__ __forceinline__ float pick_bf16(const RawBf16 &r, int i) {
   return (i & 1) ? bf_hi(x) : bf_lo(x);
 }
 
-// Statistics of one logit pair with references rt, rd (log2 domain).
+// Statistics of one logit pair with references rt, rd (log2 domain): the two
+// exponential sums, the KL accumulator sum 2^at (at - ad), and the draft
+// entropy accumulator sum 2^ad ad.
 __device__ __forceinline__ void acc_pair(float zt, float zd, float c, float rt, float rd, float &sp, float &sq,
-                                         float &a) {
+                                         float &a, float &h) {
   const float at = fmaf(zt, c, -rt), ad = fmaf(zd, c, -rd);
   const float et = fast_exp2(at), ed = fast_exp2(ad);
   sp += et;
   sq += ed;
   a = fmaf(et, at - ad, a);
+  h = fmaf(ed, ad, h);
 }
-__device__ __forceinline__ void acc_word(uint32_t t, uint32_t d, float c, float rt, float rd, float (&s)[6]) {
-  acc_pair(bf_lo(t), bf_lo(d), c, rt, rd, s[0], s[1], s[2]);
-  acc_pair(bf_hi(t), bf_hi(d), c, rt, rd, s[3], s[4], s[5]);
+// Two interleaved accumulator sets: s[0..3] and s[4..7].
+__device__ __forceinline__ void acc_word(uint32_t t, uint32_t d, float c, float rt, float rd, float (&s)[8]) {
+  acc_pair(bf_lo(t), bf_lo(d), c, rt, rd, s[0], s[1], s[2], s[3]);
+  acc_pair(bf_hi(t), bf_hi(d), c, rt, rd, s[4], s[5], s[6], s[7]);
 }
-__device__ __forceinline__ void acc_vec(uint4 t, uint4 d, float c, float rt, float rd, float (&s)[6]) {
+__device__ __forceinline__ void acc_vec(uint4 t, uint4 d, float c, float rt, float rd, float (&s)[8]) {
   acc_word(t.x, d.x, c, rt, rd, s);
   acc_word(t.y, d.y, c, rt, rd, s);
   acc_word(t.z, d.z, c, rt, rd, s);

@@ -195,13 +195,15 @@ __device__ __forceinline__ double sl_hat_of(double sf, double wvir, double sl_ma
 }
 
 // SL rule and batch cap by one workgroup (blockDim a multiple of 64, at most
-// 1024; `red_s`, `red_n` are LDS arrays of blockDim / 64 entries).  Per-thread
+// 1024; `red_s`, `red_n` are LDS arrays of blockDim / 64 entries), then the
+// per-sequence token budget (optional) bounds each next length.  Per-thread
 // fp64 partial sums, wavefront butterflies, then the wavefront totals in order:
 // a fixed order, so the cap is bitwise reproducible.  seq_err bits are OR-ed
 // atomically when `or_err` is set (fused step), else written.
 __device__ inline void block_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max,
-                                     float sl_min, int32_t sl_hi, float *sl_hat, float *sl_cap, int32_t *sl_next,
-                                     uint32_t *seq_err, bool or_err, double *red_s, int *red_n) {
+                                     float sl_min, int32_t sl_hi, const int32_t *budget, float *sl_hat,
+                                     float *sl_cap, int32_t *sl_next, uint32_t *seq_err, bool or_err, double *red_s,
+                                     int *red_n) {
   const int t = threadIdx.x, nt = blockDim.x, lane = t & 63, wave = t >> 6;
   const double lo_f = double(sl_min);
   const int32_t lo = int32_t(ceil(lo_f));
@@ -243,16 +245,20 @@ __device__ inline void block_next_sl(int32_t B, const float *sf, const float *wv
     } else {
       seq_err[b] = ok ? 0u : DSDE_ERR_SIGNAL;
     }
-    if (!ok) {
-      sl_next[b] = lo;
-      continue;
+    int32_t next = lo;
+    if (ok) {
+      const double hat = sl_hat_of(f, w, mx, lo_f);
+      const double x = hat < cap ? hat : cap;
+      double r = floor(x + 0.5);
+      r = r < double(lo) ? double(lo) : r;
+      r = r > double(sl_hi) ? double(sl_hi) : r;
+      next = int32_t(r);
     }
-    const double hat = sl_hat_of(f, w, mx, lo_f);
-    const double x = hat < cap ? hat : cap;
-    double r = floor(x + 0.5);
-    r = r < double(lo) ? double(lo) : r;
-    r = r > double(sl_hi) ? double(sl_hi) : r;
-    sl_next[b] = int32_t(r);
+    if (budget) {  // a step emits up to SL + 1 tokens (Sec. 3.2's budget clamp)
+      const int32_t room = budget[b] - 1 > 0 ? budget[b] - 1 : 0;
+      next = next < room ? next : room;
+    }
+    sl_next[b] = next;
   }
 }
 

@@ -56,28 +56,31 @@ __global__ __launch_bounds__(1024) void setup_kernel(int32_t B, int64_t N, int32
 // ---------------------------------------------------------------------------
 
 // Chunk sums of one workgroup -> one PairChunk (fixed order: lanes, then waves in fp64).
-__device__ __forceinline__ void write_pair_chunk(float rt, float rd, float sp, float sq, float a, float (*red)[kWaves],
-                                                 PairChunk *out) {
+__device__ __forceinline__ void write_pair_chunk(float rt, float rd, float sp, float sq, float a, float h,
+                                                 float (*red)[kWaves], PairChunk *out) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   sp = wave_sum(sp);
   sq = wave_sum(sq);
   a = wave_sum(a);
+  h = wave_sum(h);
   if (lane == 0) {
     red[2][wave] = sp;
     red[3][wave] = sq;
     red[4][wave] = a;
+    red[5][wave] = h;
   }
   __syncthreads();
   if (t == 0) {
     PairChunk pc;
     pc.mt = rt;
     pc.md = rd;
-    pc.sp = pc.sq = pc.a = 0.0;
+    pc.sp = pc.sq = pc.a = pc.h = 0.0;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
       pc.sp += double(red[2][w]);
       pc.sq += double(red[3][w]);
       pc.a += double(red[4][w]);
+      pc.h += double(red[5][w]);
     }
     *out = pc;
   }
@@ -118,7 +121,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
                                                              PairChunk *__restrict__ out,
                                                              Gathered *__restrict__ gathered,
                                                              ChunkArg *__restrict__ chunk_arg) {
-  __shared__ float red[5][kWaves];
+  __shared__ float red[6][kWaves];
   __shared__ uint32_t red_arg[kWaves];
   const int64_t unit = blockIdx.x;
   const int64_t k = unit / nc;
@@ -140,7 +143,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
     write_chunk_argmax<DSDE_BF16, true>(Mt, [&](int i) { return pick_bf16(rt_, i); }, chunk,
                                         chunk_arg + int64_t(w.slot) * nc + chunk, red_arg);
   const float rt = Mt * c, rd = Md * c;
-  float s[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   acc_vec(rt_.v0, rd_.v0, c, rt, rd, s);
   acc_vec(rt_.v1, rd_.v1, c, rt, rd, s);
   acc_vec(rt_.v2, rd_.v2, c, rt, rd, s);
@@ -165,7 +168,8 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
       gathered[w.slot] = Gathered{a, b};
     }
   }
-  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.slot) * nc + chunk);
+  write_pair_chunk(rt, rd, s[0] + s[4], s[1] + s[5], s[2] + s[6], s[3] + s[7], red,
+                   out + int64_t(w.slot) * nc + chunk);
 }
 
 // fp32 rows, or rows without 16-byte alignment.
@@ -177,7 +181,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
                                                                 PairChunk *__restrict__ out,
                                                                 Gathered *__restrict__ gathered,
                                                                 ChunkArg *__restrict__ chunk_arg) {
-  __shared__ float red[5][kWaves];
+  __shared__ float red[6][kWaves];
   __shared__ uint32_t red_arg[kWaves];
   const int64_t unit = blockIdx.x;
   const int64_t k = unit / nc;
@@ -205,11 +209,11 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
     write_chunk_argmax<DT, VEC>(Mt, [&](int i) { return zt[i]; }, chunk, chunk_arg + int64_t(w.slot) * nc + chunk,
                                 red_arg);
   const float rt = Mt * c, rd = Md * c;
-  float s[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < kEltsPerThread; i += 2) {
-    acc_pair(zt[i], zd[i], c, rt, rd, s[0], s[1], s[2]);
-    acc_pair(zt[i + 1], zd[i + 1], c, rt, rd, s[3], s[4], s[5]);
+    acc_pair(zt[i], zd[i], c, rt, rd, s[0], s[1], s[2], s[3]);
+    acc_pair(zt[i + 1], zd[i + 1], c, rt, rd, s[4], s[5], s[6], s[7]);
   }
   // a token outside [0, V) never matches (its sequence is flagged later)
   const int64_t local = int64_t(draft_tokens[w.pair]) - chunk * kChunk;
@@ -227,7 +231,8 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
       gathered[w.slot] = Gathered{a, b};
     }
   }
-  write_pair_chunk(rt, rd, s[0] + s[3], s[1] + s[4], s[2] + s[5], red, out + int64_t(w.slot) * nc + chunk);
+  write_pair_chunk(rt, rd, s[0] + s[4], s[1] + s[5], s[2] + s[6], s[3] + s[7], red,
+                   out + int64_t(w.slot) * nc + chunk);
 }
 
 }  // namespace

@@ -49,6 +49,7 @@ struct StepParams {
   float *kld;
   uint32_t *seq_err;
   double *row_lse;
+  float *entropy;  // draft entropy per drafted position (nats), may be null
   const PairChunk *part;
   const Gathered *gathered;
   const ChunkArg *chunk_arg;  // greedy pairs: the target row's maximum and argmax per chunk
@@ -89,13 +90,13 @@ template <int G>
 __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t slot0, int32_t s, int32_t nc,
                                      const PairChunk &q0, const ChunkArg *__restrict__ chunk_arg, ChunkArg arg0,
                                      float *st_mt, float *st_md, double *st_sp, double *st_sq, double *st_a,
-                                     int *st_bad, int *st_arg) {
+                                     double *st_h, int *st_bad, int *st_arg) {
   constexpr int P = 64 / G;  // pairs per wavefront
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane % G;
   for (int32_t base = 0; base < s; base += kSeqWaves * P) {
     const int32_t j = base + wave * P + lane / G;
     float lmt = -INFINITY, lmd = -INFINITY;
-    double lsp = 0.0, lsq = 0.0, la = 0.0;
+    double lsp = 0.0, lsq = 0.0, la = 0.0, lh = 0.0;
     // greedy: the largest raw logit among this lane's chunks and its token
     float lz = -INFINITY;
     int32_t larg = 0x7fffffff;
@@ -118,12 +119,14 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
           lsp = q.sp;
           lsq = q.sq;
           la = q.a;
+          lh = q.h;
         } else {
           const float nt = fmaxf(lmt, q.mt), nd = fmaxf(lmd, q.md);
           const double d0t = double(lmt) - nt, d0d = double(lmd) - nd;
           const double d1t = double(q.mt) - nt, d1d = double(q.md) - nd;
           const double f0t = exp2(d0t), f0d = exp2(d0d), f1t = exp2(d1t), f1d = exp2(d1d);
           la = f0t * (la + lsp * (d0t - d0d)) + f1t * (q.a + q.sp * (d1t - d1d));
+          lh = f0d * (lh + lsq * d0d) + f1d * (q.h + q.sq * d1d);
           lsp = f0t * lsp + f1t * q.sp;
           lsq = f0d * lsq + f1d * q.sq;
           lmt = nt;
@@ -132,17 +135,19 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
       }
     }
     const float mt = group_max<G>(lmt), md = group_max<G>(lmd);
-    double tsp = 0.0, tsq = 0.0, ta = 0.0;
+    double tsp = 0.0, tsq = 0.0, ta = 0.0, th = 0.0;
     if (lmt != -INFINITY) {
       const double dt = double(lmt) - double(mt), dd = double(lmd) - double(md);
       const double ft = exp2(dt), fd = exp2(dd);
       tsp = lsp * ft;
       tsq = lsq * fd;
       ta = ft * (la + lsp * (dt - dd));
+      th = fd * (lh + lsq * dd);
     }
     tsp = group_sum<G>(tsp);
     tsq = group_sum<G>(tsq);
     ta = group_sum<G>(ta);
+    th = group_sum<G>(th);
     int32_t arg = 0x7fffffff;
     if (chunk_arg) {  // the row argmax: smallest token among the chunks holding the row maximum
       const float zm = group_max<G>(lz);
@@ -156,6 +161,7 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
       st_sp[j] = tsp;
       st_sq[j] = tsq;
       st_a[j] = ta;
+      st_h[j] = th;
       st_bad[j] = !(isfinite(mt) && isfinite(md) && isfinite(tsp) && isfinite(tsq) && isfinite(ta));
       st_arg[j] = arg;
     }
@@ -366,7 +372,7 @@ __device__ inline void bonus_argmax_chunk(const char *trow, int64_t V, int64_t c
 template <int DT, bool VEC, bool FUSED>
 __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, const SignalArgs S) {
   __shared__ float st_mt[DSDE_MAX_K + 1], st_md[DSDE_MAX_K + 1];
-  __shared__ double st_sp[DSDE_MAX_K + 1], st_sq[DSDE_MAX_K + 1], st_a[DSDE_MAX_K + 1];
+  __shared__ double st_sp[DSDE_MAX_K + 1], st_sq[DSDE_MAX_K + 1], st_a[DSDE_MAX_K + 1], st_h[DSDE_MAX_K + 1];
   __shared__ int st_bad[DSDE_MAX_K + 1], st_arg[DSDE_MAX_K + 1];
   __shared__ float s_kld[64];
   __shared__ double ch_w[kMaxChunks], ch_p[kMaxChunks];
@@ -446,11 +452,14 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
   // the layout is valid, so every access stays in bounds)
   if (s > 0) {
     if (G == 16)
-      combine_pairs<16>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_bad, st_arg);
+      combine_pairs<16>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_h, st_bad,
+                        st_arg);
     else if (G == 32)
-      combine_pairs<32>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_bad, st_arg);
+      combine_pairs<32>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_h, st_bad,
+                        st_arg);
     else
-      combine_pairs<64>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_bad, st_arg);
+      combine_pairs<64>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_h, st_bad,
+                        st_arg);
   }
   __syncthreads();
   if (wave == 0) {
@@ -471,7 +480,7 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
     const float c = greedy ? kLog2e : kLog2e / T;  // the same values as the set-up's scale
     const bool active = lane < s && !err;
     bool ok = false, bad = false;
-    float my_kld = 0.f;
+    float my_kld = 0.f, my_h = 0.f;
     if (active) {
       bad = st_bad[lane] != 0;
       const double sp = st_sp[lane], sq = st_sq[lane];
@@ -479,6 +488,8 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
       // KL in log2 units: E_p[(z_t c - mt) - (z_d c - md)] - log2 S_p + log2 S_q
       const double kl = (st_a[lane] / sp - l2sp + l2sq) * kLn2;
       my_kld = kl > 0.0 ? float(kl) : 0.0f;
+      // draft entropy in log2 units: log2 S_q - E_q[z_d c - md]
+      my_h = float((l2sq - st_h[lane] / sq) * kLn2);
       // log2 p(x) - log2 q(x); z * c is exact in double
       const double lr = (double(gz.zt) * double(c) - double(st_mt[lane]) - l2sp) -
                         (double(gz.zd) * double(c) - double(st_md[lane]) - l2sq);
@@ -496,8 +507,10 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
     if (err) {
       a = 0;
       my_kld = NAN;
+      my_h = NAN;
     }
     if (lane < s) P.kld[first + lane] = my_kld;
+    if (lane < s && P.entropy) P.entropy[first + lane] = my_h;
     s_kld[lane] = my_kld;
     if (lane < width) tok[lane] = lane < a ? x : P.pad_id;
     if (lane == 0) {
@@ -877,6 +890,7 @@ int launch_verify(const VerifyArgs &a) {
   P.kld = a.kld;
   P.seq_err = a.seq_err;
   P.row_lse = a.row_lse;
+  P.entropy = a.draft_entropy;
   P.part = part;
   P.gathered = gath;
   P.chunk_arg = cargs;
@@ -894,8 +908,8 @@ int launch_verify(const VerifyArgs &a) {
   }
   if (hipGetLastError() != hipSuccess) return DSDE_DEVICE_ERROR;
   if (a.signal)
-    return launch_next_sl(a.B, S.sf, S.wvir, S.sl_max, S.sl_min, S.sl_hi, S.sl_hat, S.sl_cap, S.sl_next, a.seq_err,
-                          true, a.stream);
+    return launch_next_sl(a.B, S.sf, S.wvir, S.sl_max, S.sl_min, S.sl_hi, S.budget, S.sl_hat, S.sl_cap, S.sl_next,
+                          a.seq_err, true, a.stream);
   return DSDE_OK;
 }
 

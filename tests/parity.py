@@ -7,7 +7,7 @@ within 1e-6 probability mass of u' * Z).  Tie sequences are counted and checked
 only for validity (accepted drafts are a prefix of the drafted tokens, the rest
 is padding).
 
-Floating point: KLD within 1e-4 relative plus 1e-6 absolute.  The absolute
+Floating point: KLD and draft entropy within 1e-4 relative plus 1e-6 absolute.  The absolute
 floor comes from fp32 arithmetic: each log-probability difference entering KL
 is formed from fp32 values of magnitude up to ~10 (unit roundoff 6e-8), so a
 KL near 0 carries an absolute error of order 1e-7..1e-6.
@@ -15,6 +15,7 @@ KL near 0 carries an absolute error of order 1e-7..1e-6.
 import numpy as np
 
 KLD_REL, KLD_ABS = 1e-4, 1e-6
+ENT_REL, ENT_ABS = 1e-4, 1e-6
 LSE_ABS = 2e-5
 
 
@@ -23,7 +24,7 @@ def run_verify(dsde, step, row_lse=True):
     lse = torch.empty((max(step.N, 1), 2), dtype=torch.float64, device=step.target.device)[:step.N] \
         if row_lse else None
     out = dsde.verify(step.target, step.draft, step.sl, step.cu_sl, step.draft_tokens, step.temperature,
-                      step.u_acc, step.u_res, step.k_max, row_lse=lse)
+                      step.u_acc, step.u_res, step.k_max, row_lse=lse, draft_entropy=True)
     torch.cuda.synchronize()
     res = {k: v.cpu().numpy() for k, v in out.items()}
     if lse is not None:
@@ -110,6 +111,11 @@ def compare_verify(got, ref, sl, cu_sl, label="", host=None):
         lim = KLD_REL * np.abs(kr[pos_fine]) + KLD_ABS
         worst = int(np.argmax(d - lim))
         assert (d <= lim).all(), f"{label}: kld off by {d[worst]:.3g} (ref {kr[pos_fine][worst]:.6g})"
+    if "draft_entropy" in got and pos_fine.any():
+        eg = got["draft_entropy"].astype(np.float64)[pos_fine]
+        er = ref["entropy"][pos_fine]
+        de = np.abs(eg - er)
+        assert (de <= ENT_REL * np.abs(er) + ENT_ABS).all(), f"{label}: draft entropy off by {de.max():.3g}"
     report = {"B": B, "compared": int(cmp.sum()), "acc_ties": int((ref["acc_tie"] != 0).sum()),
               "cdf_ties": int((ref["cdf_tie"] != 0).sum()), "errored": int((~fine).sum())}
     if "row_lse" in got and pos_fine.any():

@@ -42,7 +42,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.dsde_abi_version() == 1
+    assert lib.dsde_abi_version() == 2
     for code, text in ((0, b"ok"), (1, b"invalid argument"), (2, b"workspace too small"), (3, b"device error")):
         assert lib.dsde_status_string(code) == text
     assert lib.dsde_status_string(99) == b"unknown status"
@@ -64,7 +64,7 @@ FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
 def verify_args(**over):
     a = dict(target=FAKE, draft=FAKE, dtype=1, V=1000, B=4, N=8, k_max=4, sl=FAKE, cu_sl=FAKE, toks=FAKE,
              temp=FAKE, u_acc=FAKE, u_res=FAKE, pad=-1, acc=FAKE, tokens=FAKE, kld=FAKE, err=FAKE, lse=None,
-             ws=FAKE, ws_bytes=1 << 30, stream=None)
+             ent=None, ws=FAKE, ws_bytes=1 << 30, stream=None)
     a.update(over)
     return list(a.values())
 
@@ -111,8 +111,8 @@ def test_kld_signal_rejects_invalid_arguments(lib, over):
     dict(sl_max=None), dict(hat=None), dict(cap=None), dict(nxt=None), dict(err=None),
 ])
 def test_next_sl_rejects_invalid_arguments(lib, over):
-    a = dict(B=4, sf=FAKE, wvir=FAKE, sl_max=FAKE, sl_min=2.0, sl_hi=8, hat=FAKE, cap=FAKE, nxt=FAKE, err=FAKE,
-             stream=None)
+    a = dict(B=4, sf=FAKE, wvir=FAKE, sl_max=FAKE, sl_min=2.0, sl_hi=8, budget=None, hat=FAKE, cap=FAKE, nxt=FAKE,
+             err=FAKE, stream=None)
     a.update(over)
     assert lib.dsde_next_sl(*a.values()) == 1
 
@@ -137,3 +137,24 @@ def test_stream_read_rejects_invalid_arguments(lib):
     for buf, nbytes, o in ((None, 16, out), (ok_buf, 16, None), (ok_buf, 0, out), (ok_buf, -16, out),
                            (ok_buf, 24, out), (ctypes.c_void_p(0x1008), 16, out)):
         assert fn(buf, nbytes, o, None) == 1
+
+
+@pytest.mark.parametrize("over", [
+    dict(B=0), dict(N=-1), dict(sl=None), dict(cu=None), dict(acc=None), dict(err=None), dict(amax=None),
+    dict(ksum=None), dict(kcnt=None), dict(kmax=None), dict(kld=None),
+])
+def test_calibration_update_rejects_invalid_arguments(lib, over):
+    a = dict(B=4, N=8, sl=FAKE, cu=FAKE, acc=FAKE, kld=FAKE, err=FAKE, amax=FAKE, ksum=FAKE, kcnt=FAKE, kmax=FAKE,
+             stream=None)
+    a.update(over)
+    assert lib.dsde_calibration_update(*a.values()) == 1
+
+
+@pytest.mark.parametrize("over", [
+    dict(B=0), dict(eps=-1e-6), dict(eps=float("nan")), dict(pooled=2), dict(amax=None), dict(ksum=None),
+    dict(kcnt=None), dict(kmax=None), dict(out=None),
+])
+def test_calibrate_sl_max_rejects_invalid_arguments(lib, over):
+    a = dict(B=4, amax=FAKE, ksum=FAKE, kcnt=FAKE, kmax=FAKE, eps=1e-6, pooled=0, out=FAKE, stream=None)
+    a.update(over)
+    assert lib.dsde_calibrate_sl_max(*a.values()) == 1

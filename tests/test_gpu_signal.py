@@ -127,6 +127,16 @@ def test_next_sl_alone(gpu_lib):
     ok = ties == 0
     assert np.array_equal(got["sl_next"][ok], ref["sl_next"][ok])
     print(f"[report] next_sl ties={int(ties.sum())} of {B}", flush=True)
+    # the per-sequence token budget (Sec. 3.2): min(SL_next, max(budget - 1, 0))
+    budget = rng.integers(-2, 20, B).astype(np.int32)
+    out_b = gpu_lib.next_sl(dev(sf), dev(wvir), dev(sl_max), 2.0, 16, budget=dev(budget))
+    torch.cuda.synchronize()
+    ref_b = oracle.next_sl(sf.astype(np.float64), wvir.astype(np.float64), sl_max.astype(np.float64), 2.0, 16,
+                           budget=budget)
+    nb = out_b["sl_next"].cpu().numpy()
+    tight = budget - 1 <= 2  # the budget decides, whatever the rounding
+    assert np.array_equal(nb[ok | tight], ref_b["sl_next"][ok | tight])
+    assert np.array_equal(out_b["sl_cap"].cpu().numpy(), out["sl_cap"].cpu().numpy())
 
 
 def oracle_chain(host, h0, hd0, c0, smax, sl_hi):
@@ -225,17 +235,19 @@ def test_fused_step_equals_the_three_calls(gpu_lib, name):
     st = W.make_signal_state(cfg, seed=31, device="cuda")
     announce(f"fused step vs chain {name}")
     st_a, st_b = clone_state(st), clone_state(st)
+    budget = torch.as_tensor(np.random.default_rng(3).integers(0, 10, step.B).astype(np.int32), device="cuda")
     v = gpu_lib.verify(step.target, step.draft, step.sl, step.cu_sl, step.draft_tokens, step.temperature,
-                       step.u_acc, step.u_res, step.k_max)
+                       step.u_acc, step.u_res, step.k_max, draft_entropy=True)
     s_ = gpu_lib.kld_signal(step.sl, step.cu_sl, v["kld"], st_a.hist, st_a.head, st_a.count)
-    n_ = gpu_lib.next_sl(s_["sf"], s_["wvir"], st_a.sl_max, 2.0, step.k_max)
+    n_ = gpu_lib.next_sl(s_["sf"], s_["wvir"], st_a.sl_max, 2.0, step.k_max, budget=budget)
     f = gpu_lib.step(step.target, step.draft, step.sl, step.cu_sl, step.draft_tokens, step.temperature,
-                     step.u_acc, step.u_res, step.k_max, st_b.hist, st_b.head, st_b.count, st_b.sl_max)
+                     step.u_acc, step.u_res, step.k_max, st_b.hist, st_b.head, st_b.count, st_b.sl_max,
+                     draft_entropy=True, budget=budget)
     torch.cuda.synchronize()
     chain = {**v, **s_, **n_}
     for k in ("accepted", "tokens", "sl_next"):
         assert torch.equal(chain[k], f[k]), k
-    for k in ("kld", "mu_last", "var_short", "var_long", "wvir", "sf", "sl_hat", "sl_cap"):
+    for k in ("kld", "draft_entropy", "mu_last", "var_short", "var_long", "wvir", "sf", "sl_hat", "sl_cap"):
         assert torch.equal(chain[k].view(torch.int32), f[k].view(torch.int32)), k
     assert torch.equal(st_a.hist.view(torch.int32), st_b.hist.view(torch.int32))
     assert torch.equal(st_a.head, st_b.head) and torch.equal(st_a.count, st_b.count)
@@ -297,3 +309,47 @@ def test_resume_from_snapshot(gpu_lib):
         sl, sigma = f["sl_next"].cpu().numpy(), W.walk_sigma(sigma, cfg, seed, t)
     assert torch.equal(st2.hist.view(torch.int32), st.hist.view(torch.int32))
     assert torch.equal(st2.head, st.head) and torch.equal(st2.count, st.count)
+
+
+@pytest.mark.parametrize("name", ["b64", "greedy"])
+def test_sl_max_calibration(gpu_lib, name):
+    """Eq. 1 over four calibration steps, per sequence and pooled, against the
+    oracle's Eq. 1 on the oracle's own verification of the same inputs
+    (sequences with an acceptance or draw tie in any step are left out)."""
+    cfg = W.CONFIGS[name]
+    announce(f"SL_max calibration {name}")
+    B = cfg["B"]
+    state = gpu_lib.new_calibration_state(B)
+    acc_ref = [[] for _ in range(B)]
+    kld_ref = [[] for _ in range(B)]
+    tie = np.zeros(B, bool)
+    for t in range(4):
+        step = W.make_step(cfg, seed=70 + t, device="cuda")
+        v = gpu_lib.verify(step.target, step.draft, step.sl, step.cu_sl, step.draft_tokens, step.temperature,
+                           step.u_acc, step.u_res, step.k_max)
+        gpu_lib.calibration_update(step.sl, step.cu_sl, v["accepted"], v["kld"], v["seq_err"], state)
+        host = W.host_arrays(step)
+        ref = oracle.verify(**host, n_threads=16)
+        tie |= ref["acc_tie"] != 0  # a draw tie changes the emitted token, not the count
+        cu = host["cu_sl"]
+        for b in range(B):
+            acc_ref[b].append(int(ref["accepted"][b]))
+            kld_ref[b].extend(ref["kld"][cu[b]:cu[b + 1]].tolist())
+    per = gpu_lib.calibrate_sl_max(state, eps=1e-6).cpu().numpy()
+    pooled = gpu_lib.calibrate_sl_max(state, eps=1e-6, pooled=True).cpu().numpy()
+    want = np.array([oracle.calibrate_sl_max(acc_ref[b], kld_ref[b]) for b in range(B)])
+    ok = ~tie
+    np.testing.assert_allclose(per[ok], want[ok], rtol=1e-4)
+    # pooled: the KLD part does not depend on the acceptance decisions, and the
+    # pooled SL_A,max is fixed whenever no tie can move the batch maximum
+    allk = [k for b in range(B) for k in kld_ref[b]]
+    a_free = max(max(acc_ref[b]) for b in range(B) if ok[b])
+    a_all = max(max(a) for a in acc_ref)
+    if not tie.any() or a_free == cfg["k_max"]:
+        want_pooled = oracle.calibrate_sl_max([a_all if not tie.any() else a_free], allk)
+        np.testing.assert_allclose(pooled, want_pooled, rtol=1e-4)
+    else:
+        print(f"[report] calibration {name}: pooled value left unchecked (tie at the maximum)", flush=True)
+    assert np.all(pooled == pooled[0])
+    print(f"[report] calibration {name}: compared {int(ok.sum())} of {B}, pooled SL_max {pooled[0]:.4f}",
+          flush=True)
