@@ -1,9 +1,10 @@
 // Streaming-read ceiling: a plain read-reduce kernel with the statistics
-// pass's access pattern (16-byte vector loads, each wavefront load 1 KiB
-// contiguous) and no arithmetic beyond one XOR per word.  What it reaches over
+// pass's access pattern (16-byte streaming vector loads, each wavefront load
+// 1 KiB contiguous) and no arithmetic beyond one XOR per word.  What it reaches over
 // a buffer much larger than the last-level cache is the read bandwidth the
 // statistics pass is measured against.
 #include "common.hpp"
+#include "row_io.hpp"
 
 namespace dsde {
 namespace {
@@ -22,7 +23,7 @@ __global__ __launch_bounds__(kProbeThreads) void stream_read_kernel(const uint4 
 #pragma unroll
   for (int u = 0; u < kProbeLoads; ++u) {
     const int64_t i = base + int64_t(u) * kProbeThreads;
-    v[u] = p[i < n ? i : n - 1];  // clamped: always in bounds
+    v[u] = stream_load(p + (i < n ? i : n - 1));  // clamped: always in bounds
   }
   uint32_t acc = 0;
 #pragma unroll

@@ -18,6 +18,20 @@ constexpr float kPadF32 = -7.9228162514264337593543950336e28f;  // -2^96
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// Streaming 16-byte loads (the nontemporal hint): logit rows are read once per
+// pass, and with the hint a plain read of a buffer far larger than the caches
+// runs about 10% faster on this part than with ordinary loads.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 stream_load(const uint4 *p) {
+  const u32x4_t w = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+  return make_uint4(w.x, w.y, w.z, w.w);
+}
+__device__ __forceinline__ float4 stream_load(const float4 *p) {
+  const f32x4_t w = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t *>(p));
+  return make_float4(w.x, w.y, w.z, w.w);
+}
+
 // 2^x on the transcendental unit (about 1 ulp; results below 2^-126 flush to 0).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -103,8 +117,8 @@ __device__ __forceinline__ RawBf16 load_raw_bf16(const void *row, int64_t V, int
   const int64_t last = V / 8 - 1;
   const int64_t i0 = chunk * 1024 + t;
   const uint4 pad = make_uint4(kPadBf16x2, kPadBf16x2, kPadBf16x2, kPadBf16x2);
-  const uint4 a0 = p[min(i0, last)], a1 = p[min(i0 + 256, last)];
-  const uint4 a2 = p[min(i0 + 512, last)], a3 = p[min(i0 + 768, last)];
+  const uint4 a0 = stream_load(p + min(i0, last)), a1 = stream_load(p + min(i0 + 256, last));
+  const uint4 a2 = stream_load(p + min(i0 + 512, last)), a3 = stream_load(p + min(i0 + 768, last));
   RawBf16 r;
   r.v0 = i0 <= last ? a0 : pad;
   r.v1 = i0 + 256 <= last ? a1 : pad;
@@ -161,7 +175,7 @@ __device__ __forceinline__ void load_chunk_f32(const void *row, int64_t V, int64
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
       const int64_t i = chunk * 2048 + g * 256 + t;
-      const float4 w = p[min(i, last)];
+      const float4 w = stream_load(p + min(i, last));
       const bool ok = i <= last;
       z[g * 4 + 0] = ok ? w.x : kPadF32;
       z[g * 4 + 1] = ok ? w.y : kPadF32;
