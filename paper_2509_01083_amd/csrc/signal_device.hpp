@@ -194,12 +194,18 @@ __device__ __forceinline__ double sl_hat_of(double sf, double wvir, double sl_ma
   return pen <= 1.0 ? (1.0 - pen) * (sl_max - sl_min) + sl_min : sl_min;
 }
 
+// Sequences per thread whose inputs block_next_sl keeps in registers between
+// its two passes (one memory round trip); larger batches load them twice.
+constexpr int kNextSlRegs = 4;
+
 // SL rule and batch cap by one workgroup (blockDim a multiple of 64, at most
 // 1024; `red_s`, `red_n` are LDS arrays of blockDim / 64 entries), then the
 // per-sequence token budget (optional) bounds each next length.  Per-thread
 // fp64 partial sums, wavefront butterflies, then the wavefront totals in order:
 // a fixed order, so the cap is bitwise reproducible.  seq_err bits are OR-ed
-// atomically when `or_err` is set (fused step), else written.
+// into what earlier kernels wrote when `or_err` is set (fused step), else
+// written.
+
 __device__ inline void block_next_sl(int32_t B, const float *sf, const float *wvir, const float *sl_max,
                                      float sl_min, int32_t sl_hi, const int32_t *budget, float *sl_hat,
                                      float *sl_cap, int32_t *sl_next, uint32_t *seq_err, bool or_err, double *red_s,
@@ -207,18 +213,49 @@ __device__ inline void block_next_sl(int32_t B, const float *sf, const float *wv
   const int t = threadIdx.x, nt = blockDim.x, lane = t & 63, wave = t >> 6;
   const double lo_f = double(sl_min);
   const int32_t lo = int32_t(ceil(lo_f));
+  const bool cached = B <= kNextSlRegs * nt;
+  // pass 1: SL_hat of every sequence (thread t: sequences t, t + nt, ...);
+  // with a small batch every input of both passes is loaded here at once
+  float r_f[kNextSlRegs], r_w[kNextSlRegs], r_m[kNextSlRegs];
+  int32_t r_bud[kNextSlRegs];
+  uint32_t r_err[kNextSlRegs];
+  if (cached) {
+#pragma unroll
+    for (int i = 0; i < kNextSlRegs; ++i) {
+      const int32_t b = t + i * nt;
+      r_f[i] = b < B ? sf[b] : 0.f;
+      r_w[i] = b < B ? wvir[b] : 0.f;
+      r_m[i] = b < B ? sl_max[b] : 0.f;
+      r_bud[i] = b < B && budget ? budget[b] : 0;
+      r_err[i] = b < B && or_err ? seq_err[b] : 0u;
+    }
+  }
   double part = 0.0;
   int cnt = 0;
-  for (int32_t b = t; b < B; b += nt) {
-    const double f = sf[b], w = wvir[b], mx = sl_max[b];
-    const bool ok = isfinite(f) && isfinite(w) && isfinite(mx) && mx >= lo_f;
-    if (ok) {
-      const double hat = sl_hat_of(f, w, mx, lo_f);
-      sl_hat[b] = float(hat);
+  if (cached) {
+#pragma unroll
+    for (int i = 0; i < kNextSlRegs; ++i) {
+      const int32_t b = t + i * nt;
+      if (b >= B) continue;
+      const double f = r_f[i], w = r_w[i], mx = r_m[i];
+      const bool ok = isfinite(f) && isfinite(w) && isfinite(mx) && mx >= lo_f;
+      const double hat = ok ? sl_hat_of(f, w, mx, lo_f) : 0.0;
+      sl_hat[b] = ok ? float(hat) : NAN;
       part += hat;
-      ++cnt;
-    } else {
-      sl_hat[b] = NAN;
+      cnt += ok;
+    }
+  } else {
+    for (int32_t b = t; b < B; b += nt) {
+      const double f = sf[b], w = wvir[b], mx = sl_max[b];
+      const bool ok = isfinite(f) && isfinite(w) && isfinite(mx) && mx >= lo_f;
+      if (ok) {
+        const double hat = sl_hat_of(f, w, mx, lo_f);
+        sl_hat[b] = float(hat);
+        part += hat;
+        ++cnt;
+      } else {
+        sl_hat[b] = NAN;
+      }
     }
   }
   part = wave_sum_f64(part);
@@ -237,14 +274,12 @@ __device__ inline void block_next_sl(int32_t B, const float *sf, const float *wv
   }
   const double cap = n > 0 ? total / double(n) : NAN;
   if (t == 0) sl_cap[0] = float(cap);
-  for (int32_t b = t; b < B; b += nt) {
-    const double f = sf[b], w = wvir[b], mx = sl_max[b];
+  // pass 2: the rounded, clamped next length under the cap
+  auto next_of = [&](int32_t b, double f, double w, double mx, int32_t bud, uint32_t err) {
     const bool ok = isfinite(f) && isfinite(w) && isfinite(mx) && mx >= lo_f;
-    if (or_err) {
-      if (!ok) atomicOr(&seq_err[b], DSDE_ERR_SIGNAL);
-    } else {
-      seq_err[b] = ok ? 0u : DSDE_ERR_SIGNAL;
-    }
+    // or_err: only this thread writes seq_err[b] in this kernel, so a plain
+    // read-modify-write adds the signal bit to what earlier kernels set
+    seq_err[b] = or_err ? (ok ? err : err | DSDE_ERR_SIGNAL) : (ok ? 0u : DSDE_ERR_SIGNAL);
     int32_t next = lo;
     if (ok) {
       const double hat = sl_hat_of(f, w, mx, lo_f);
@@ -255,10 +290,20 @@ __device__ inline void block_next_sl(int32_t B, const float *sf, const float *wv
       next = int32_t(r);
     }
     if (budget) {  // a step emits up to SL + 1 tokens (Sec. 3.2's budget clamp)
-      const int32_t room = budget[b] - 1 > 0 ? budget[b] - 1 : 0;
+      const int32_t room = bud - 1 > 0 ? bud - 1 : 0;
       next = next < room ? next : room;
     }
     sl_next[b] = next;
+  };
+  if (cached) {
+#pragma unroll
+    for (int i = 0; i < kNextSlRegs; ++i) {
+      const int32_t b = t + i * nt;
+      if (b < B) next_of(b, r_f[i], r_w[i], r_m[i], r_bud[i], r_err[i]);
+    }
+  } else {
+    for (int32_t b = t; b < B; b += nt)
+      next_of(b, sf[b], wvir[b], sl_max[b], budget ? budget[b] : 0, or_err ? seq_err[b] : 0u);
   }
 }
 

@@ -25,11 +25,25 @@ __global__ __launch_bounds__(1024) void setup_kernel(int32_t B, int64_t N, int32
                                                      const float *__restrict__ temperature,
                                                      uint32_t *__restrict__ seq_err, WorkItem *__restrict__ work) {
   const int t = threadIdx.x;
+  // a batch of at most blockDim sequences (thread t: sequence t) is checked and
+  // listed from values loaded once; larger batches loop and load twice
+  const bool one = B <= int32_t(blockDim.x);
   const int64_t c_first = cu_sl[0], c_last = cu_sl[B];
+  int32_t s0 = 0, f0 = 0;
+  float T0 = 1.0f;
   int bad = 0;
-  for (int32_t b = t; b < B; b += blockDim.x) {
-    const int64_t s = sl[b];
-    if (s < 0 || s > k_max || int64_t(cu_sl[b + 1]) - int64_t(cu_sl[b]) != s) bad = 1;
+  if (one) {
+    if (t < B) {
+      s0 = sl[t];
+      f0 = cu_sl[t];
+      T0 = temperature[t];
+      if (s0 < 0 || s0 > k_max || int64_t(cu_sl[t + 1]) - int64_t(f0) != s0) bad = 1;
+    }
+  } else {
+    for (int32_t b = t; b < B; b += blockDim.x) {
+      const int64_t s = sl[b];
+      if (s < 0 || s > k_max || int64_t(cu_sl[b + 1]) - int64_t(cu_sl[b]) != s) bad = 1;
+    }
   }
   bad = __syncthreads_or(bad);
   if (c_first != 0 || c_last != N) bad = 1;
@@ -38,16 +52,19 @@ __global__ __launch_bounds__(1024) void setup_kernel(int32_t B, int64_t N, int32
     for (int64_t k = t; k < N; k += blockDim.x) work[k] = WorkItem{int32_t(k), -1, 0u, -1};
     return;
   }
-  for (int32_t b = t; b < B; b += blockDim.x) {
-    const int32_t first = cu_sl[b], s = sl[b];
+  // the same expression as every later kernel's scale; a temperature outside
+  // the admissible range is flagged by the acceptance kernel.  T = 0 selects
+  // greedy verification: statistics at T = 1, and the sign bit asks the
+  // statistics kernel for the chunk argmax of the target row.
+  auto list = [&](int32_t b, int32_t first, int32_t s, float T) {
     seq_err[b] = 0u;
-    // the same expression as every later kernel's scale; a temperature outside
-    // the admissible range is flagged by the acceptance kernel.  T = 0 selects
-    // greedy verification: statistics at T = 1, and the sign bit asks the
-    // statistics kernel for the chunk argmax of the target row.
-    const float T = temperature[b];
     const uint32_t cbits = T == 0.0f ? (__float_as_uint(kLog2e) | kGreedyBit) : __float_as_uint(kLog2e / T);
     for (int32_t j = 0; j < s; ++j) work[first + j] = WorkItem{first + j, first + b + j, cbits, b * k_max + j};
+  };
+  if (one) {
+    if (t < B) list(t, f0, s0, T0);
+  } else {
+    for (int32_t b = t; b < B; b += blockDim.x) list(b, cu_sl[b], sl[b], temperature[b]);
   }
 }
 

@@ -32,7 +32,7 @@ namespace {
 constexpr int kSeqThreads = 512;              // 8 wavefronts per sequence
 constexpr int kSeqWaves = kSeqThreads / 64;
 constexpr int kVirt = kThreads / 64;          // chunk-layout threads played by one lane (4)
-constexpr int kSignalWave = 1;                // wavefront that runs the fused signal update
+constexpr int kSignalWave = kSeqWaves - 1;    // wavefront that runs the fused signal update
 
 // How many of a lane's chunk-layout threads one loop iteration handles: as
 // many as the registers allow loads in flight for.
@@ -367,8 +367,9 @@ __device__ inline void bonus_argmax_chunk(const char *trow, int64_t V, int64_t c
 //   2. wavefront w: the draw-weight totals of chunks w, w + 8, ... (residual
 //      max(0, p - q) of the first rejected pair, or the bonus row), into LDS.
 //   3. wavefront 0: fixed-order fp64 prefix over the chunk totals to the chunk
-//      holding u' * Z, then the ordered scan inside it.  Fused: wavefront 1
-//      meanwhile runs the signal update of the sequence.
+//      holding u' * Z, then the ordered scan inside it.
+//   Fused: the last wavefront runs the signal update of the sequence between
+//   steps 1 and 2.
 template <int DT, bool VEC, bool FUSED>
 __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, const SignalArgs S) {
   __shared__ float st_mt[DSDE_MAX_K + 1], st_md[DSDE_MAX_K + 1];
@@ -552,6 +553,18 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
   __syncthreads();
   const DrawJob job = s_job;
 
+  if constexpr (FUSED) {
+    if (wave == kSignalWave) {
+      // the signal update of Sec. 3.1.2 on the KLD values just computed, before
+      // this wavefront's share of the draw stream (the last wavefront has the
+      // fewest chunks), so that it is off the path of the chunk search
+      const uint32_t e = wave_signal_update(s, first, nullptr, s_kld[lane], rp, S.hist + int64_t(b) * S.W,
+                                            S.head + b, S.count + b, S.W, S.n_short, S.n_long, S.delta, S.eps,
+                                            S.mu_last + b, S.var_short + b, S.var_long + b, S.wvir + b, S.sf + b);
+      if (e && lane == 0) atomicOr(&P.seq_err[b], e);
+    }
+  }
+
   // ---- 2. draw-weight totals of every chunk
   const size_t esz = DT == DSDE_BF16 ? 2 : 4;
   const int32_t nc = P.nc;
@@ -606,16 +619,6 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
     }
   }
 
-  if constexpr (FUSED) {
-    if (wave == kSignalWave) {
-      // the signal update of Sec. 3.1.2 on the KLD values just computed
-      // (concurrent with the chunk search of wavefront 0)
-      const uint32_t e = wave_signal_update(s, first, nullptr, s_kld[lane], rp, S.hist + int64_t(b) * S.W,
-                                            S.head + b, S.count + b, S.W, S.n_short, S.n_long, S.delta, S.eps,
-                                            S.mu_last + b, S.var_short + b, S.var_long + b, S.wvir + b, S.sf + b);
-      if (e && lane == 0) atomicOr(&P.seq_err[b], e);
-    }
-  }
   if (job.kind < 0 || job.kind == 2) {  // flagged, or a greedy token already emitted
     if (err && wave == 0 && lane == 0) atomicOr(&P.seq_err[b], err);
     return;

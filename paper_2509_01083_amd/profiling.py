@@ -40,6 +40,8 @@ def kernel_source_hash():
 def short_name(name):
     m = re.search(r"dsde::\(anonymous namespace\)::(\w+)(<[^>(]*>)?", name)
     if m:
+        if m.group(1) == KERNEL:  # the statistics kernel under one name, whatever its template arguments
+            return KERNEL
         return m.group(1) + (m.group(2) or "")
     if CALIBRATION_KERNEL in name:
         return CALIBRATION_KERNEL
