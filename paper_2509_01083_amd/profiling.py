@@ -81,15 +81,40 @@ def median(v):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace", required=True)
-    ap.add_argument("--fetch", required=True)
-    ap.add_argument("--write", required=True)
+    ap.add_argument("--fetch", help="FETCH_SIZE counter CSV (omitted: durations only)")
+    ap.add_argument("--write", help="WRITE_SIZE counter CSV")
     ap.add_argument("--workload", default="b256")
-    ap.add_argument("--algorithmic-bytes", type=float, required=True)
-    ap.add_argument("--json", required=True)
+    ap.add_argument("--algorithmic-bytes", type=float)
+    ap.add_argument("--json", help="traffic file to write (needs the counters)")
     ap.add_argument("--md", required=True)
     ap.add_argument("--command", action="append", default=[])
     ap.add_argument("--bench-log", help="output of bench.py run without the profiler (its last line is the JSON)")
     a = ap.parse_args()
+    bench = None
+    if a.bench_log:
+        with open(a.bench_log) as f:
+            bench = json.loads(f.read().strip().splitlines()[-1])
+    cfg = bench["config"] if bench else {}
+    shape = ", ".join(f"{k}={cfg[k]}" for k in ("B", "N", "V") if k in cfg)
+    lines = [f"# {KERNEL}, workload {a.workload}" + (f" ({shape}, bf16)" if shape else ""), "",
+             "Commands (from the repository root):", ""]
+    lines += [f"    {c}" for c in a.command]
+    lines += ["", "## Kernel durations (rocprofv3 --kernel-trace --stats)", "",
+              "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
+    for k, n, avg, lo, hi in trace_stats(a.trace):
+        lines.append(f"| {k} | {n} | {avg:.2f} | {lo:.2f} | {hi:.2f} |")
+    if not (a.fetch and a.write):
+        if bench and "loop" in bench:
+            lp = bench["loop"]
+            lines += ["", "## Controller loop (bench.py without the profiler)", "",
+                      f"Per step: mean {lp['ms_per_step']['mean'] * 1e3:.1f} us, median "
+                      f"{lp['ms_per_step']['median'] * 1e3:.1f} us, p95 {lp['ms_per_step']['p95'] * 1e3:.1f} us; "
+                      f"mean SL {lp['mean_sl']['mean']:.2f}; cap {lp['sl_cap']['mean']:.2f}; "
+                      f"{lp['fraction_in_sl_min_branch'] * 100:.0f}% of sequences in the SL_min branch; "
+                      f"{bench['value'] / 1e6:.2f} M rows/s over all steps.", ""]
+        with open(a.md, "w") as f:
+            f.write("\n".join(lines))
+        return
     fetch = counter_values(a.fetch, "FETCH_SIZE")
     write = counter_values(a.write, "WRITE_SIZE")
     f_cal = median(fetch[CALIBRATION_KERNEL]) * 1024 / CALIBRATION_BYTES
@@ -100,15 +125,10 @@ def main():
                "fetch_bytes_per_launch": f_k, "write_bytes_per_launch": w_k, "bytes_per_launch": f_k + w_k,
                "fetch_counter_scale": 1.0 / f_cal, "write_counter_scale": 1.0 / w_cal,
                "algorithmic_bytes": a.algorithmic_bytes}
-    with open(a.json, "w") as f:
-        json.dump(traffic, f, indent=1)
-        f.write("\n")
-    lines = [f"# {KERNEL}, workload {a.workload} (B=256, V=128256 bf16)", "", "Commands (from the repository root):", ""]
-    lines += [f"    {c}" for c in a.command]
-    lines += ["", "## Kernel durations (rocprofv3 --kernel-trace --stats)", "",
-              "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
-    for k, n, avg, lo, hi in trace_stats(a.trace):
-        lines.append(f"| {k} | {n} | {avg:.2f} | {lo:.2f} | {hi:.2f} |")
+    if a.json:
+        with open(a.json, "w") as f:
+            json.dump(traffic, f, indent=1)
+            f.write("\n")
     lines += ["", "## HBM traffic per launch (rocprofv3 --pmc, one counter per run)", "",
               f"Calibration: {CALIBRATION_KERNEL} over 1 GiB reads FETCH_SIZE = "
               f"{median(fetch[CALIBRATION_KERNEL]):.0f} KiB and WRITE_SIZE = {median(write[CALIBRATION_KERNEL]):.0f} KiB "
@@ -120,9 +140,8 @@ def main():
             continue
         fr, wr = median(fetch[k]), median(write[k])
         lines.append(f"| {k} | {fr:.0f} | {wr:.0f} | {fr * 1024 / f_cal / 1e6:.2f} | {wr * 1024 / w_cal / 1e6:.3f} |")
-    if a.bench_log:
-        with open(a.bench_log) as f:
-            r = json.loads(f.read().strip().splitlines()[-1])
+    if bench:
+        r = bench
         ev_us = r["roofline"]["kernel_ms"] * 1e3
         tr_us = [avg for k, _, avg, _, _ in trace_stats(a.trace) if k == KERNEL][0]
         lines += ["", "## HIP events against the trace", "",

@@ -228,9 +228,14 @@ def clone_state(st):
                          sl_max=st.sl_max.clone())
 
 
-@pytest.mark.parametrize("name", ["tiny", "b64", "b256", "greedy"])
+# more sequences than the set-up kernel and the cap kernel hold in registers
+# (their looping paths), half of them greedy
+WIDE = dict(W.CONFIGS["greedy"], B=1500, V=512)
+
+
+@pytest.mark.parametrize("name", ["tiny", "b64", "b256", "greedy", "wide"])
 def test_fused_step_equals_the_three_calls(gpu_lib, name):
-    cfg = W.CONFIGS[name]
+    cfg = WIDE if name == "wide" else W.CONFIGS[name]
     step = W.make_step(cfg, seed=31, device="cuda")
     st = W.make_signal_state(cfg, seed=31, device="cuda")
     announce(f"fused step vs chain {name}")

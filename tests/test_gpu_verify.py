@@ -82,6 +82,19 @@ def test_large_vocab(gpu_lib, V, dtype):
     check_step(gpu_lib, step, f"large vocab V={V} {dtype}")
 
 
+def test_large_batch(gpu_lib):
+    """More sequences than the set-up kernel has threads (its looping path),
+    ragged SL including 0, mixed temperatures and greedy sequences."""
+    rng = np.random.default_rng(1500)
+    B, V = 1500, 300
+    sls = rng.integers(0, 4, B).tolist()
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V, noise=0.8)
+    temps = rng.choice([0.0, 0.7, 1.0, 1.3], B).tolist()
+    step = step_from_arrays(target, draft, sls, tokens, temps, u_acc, u_res, 3)
+    _, _, rep = check_step(gpu_lib, step, f"large batch B={B}")
+    assert rep["compared"] >= 0.9 * B
+
+
 def test_nothing_drafted(gpu_lib):
     rng = np.random.default_rng(3)
     V = 5000
