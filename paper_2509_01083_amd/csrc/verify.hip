@@ -29,10 +29,12 @@ namespace {
 // per-sequence kernel: acceptance, draw weights and draw
 // ---------------------------------------------------------------------------
 
-constexpr int kSeqThreads = 512;              // 8 wavefronts per sequence
-constexpr int kSeqWaves = kSeqThreads / 64;
+// Threads per sequence: 512 (8 wavefronts) when every sequence has a CU of its
+// own, 256 when sequences outnumber the CUs (then three workgroups share a CU
+// and each one's latency-bound phases overlap the others' row streams).
+constexpr int kSeqThreadsWide = 512;
+constexpr int kSeqThreadsNarrow = 256;
 constexpr int kVirt = kThreads / 64;          // chunk-layout threads played by one lane (4)
-constexpr int kSignalWave = kSeqWaves - 1;    // wavefront that runs the fused signal update
 
 // How many of a lane's chunk-layout threads one loop iteration handles: as
 // many as the registers allow loads in flight for.
@@ -86,14 +88,14 @@ __device__ __forceinline__ double group_sum(double v) {
 // Combines the chunk partials of every drafted pair of one sequence (stored
 // under slots slot0 + j): groups of G lanes, one pair per group, lane g of a
 // group folds chunks g, g + G, ...  Results go to LDS (st_*[j] for position j).
-template <int G>
+template <int G, int WAVES>
 __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t slot0, int32_t s, int32_t nc,
                                      const PairChunk &q0, const ChunkArg *__restrict__ chunk_arg, ChunkArg arg0,
                                      float *st_mt, float *st_md, double *st_sp, double *st_sq, double *st_a,
                                      double *st_h, int *st_bad, int *st_arg) {
   constexpr int P = 64 / G;  // pairs per wavefront
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane % G;
-  for (int32_t base = 0; base < s; base += kSeqWaves * P) {
+  for (int32_t base = 0; base < s; base += WAVES * P) {
     const int32_t j = base + wave * P + lane / G;
     float lmt = -INFINITY, lmd = -INFINITY;
     double lsp = 0.0, lsq = 0.0, la = 0.0, lh = 0.0;
@@ -370,8 +372,11 @@ __device__ inline void bonus_argmax_chunk(const char *trow, int64_t V, int64_t c
 //      holding u' * Z, then the ordered scan inside it.
 //   Fused: the last wavefront runs the signal update of the sequence between
 //   steps 1 and 2.
-template <int DT, bool VEC, bool FUSED>
-__global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, const SignalArgs S) {
+template <int DT, bool VEC, bool FUSED, int NT>
+__global__ __launch_bounds__(NT) void seq_kernel(const StepParams P, const SignalArgs S) {
+  constexpr int kSeqThreads = NT;
+  constexpr int kSeqWaves = NT / 64;
+  constexpr int kSignalWave = kSeqWaves - 1;  // wavefront that runs the fused signal update
   __shared__ float st_mt[DSDE_MAX_K + 1], st_md[DSDE_MAX_K + 1];
   __shared__ double st_sp[DSDE_MAX_K + 1], st_sq[DSDE_MAX_K + 1], st_a[DSDE_MAX_K + 1], st_h[DSDE_MAX_K + 1];
   __shared__ int st_bad[DSDE_MAX_K + 1], st_arg[DSDE_MAX_K + 1];
@@ -453,14 +458,14 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
   // the layout is valid, so every access stays in bounds)
   if (s > 0) {
     if (G == 16)
-      combine_pairs<16>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_h, st_bad,
-                        st_arg);
+      combine_pairs<16, kSeqWaves>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a,
+                                    st_h, st_bad, st_arg);
     else if (G == 32)
-      combine_pairs<32>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_h, st_bad,
-                        st_arg);
+      combine_pairs<32, kSeqWaves>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a,
+                                    st_h, st_bad, st_arg);
     else
-      combine_pairs<64>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a, st_h, st_bad,
-                        st_arg);
+      combine_pairs<64, kSeqWaves>(P.part, slot0, s, P.nc, q0, cargs, arg0, st_mt, st_md, st_sp, st_sq, st_a,
+                                    st_h, st_bad, st_arg);
   }
   __syncthreads();
   if (wave == 0) {
@@ -752,7 +757,7 @@ __global__ __launch_bounds__(kSeqThreads) void seq_kernel(const StepParams P, co
   const double rem = s_rem;
   const float ref = s_ref;
   const char *trow = (const char *)P.target + size_t(job.target_row) * size_t(P.V) * esz;
-  constexpr int kRun = kChunk / kSeqThreads;  // 16
+  constexpr int kRun = kChunk / kSeqThreads;  // 16 or 32
   const int64_t run0 = chunk * kChunk + int64_t(kRun) * t;
   float w[kRun];
   {
@@ -845,22 +850,33 @@ static size_t spread_lds(K kernel) {
 
 template <int DT, bool VEC>
 static void launch_seq(const VerifyArgs &a, const StepParams &P, const SignalArgs &S) {
-  // Two workgroups fit on one CU.  With no more sequences than CUs the
-  // dispatcher could still pair them up on half of the CUs, each pair then
-  // sharing one CU's load bandwidth; reserving more than half of the CU's LDS
-  // per workgroup (unused) places one sequence per CU.
-  static const size_t spread_fused = spread_lds(seq_kernel<DT, VEC, true>);
-  static const size_t spread_plain = spread_lds(seq_kernel<DT, VEC, false>);
+  // With no more sequences than CUs: 512 threads per sequence, one sequence
+  // per CU.  Two such workgroups would fit on one CU, and the dispatcher could
+  // pair them up on half of the CUs, each pair then sharing one CU's load
+  // bandwidth; reserving more than half of the CU's LDS per workgroup (unused)
+  // places one sequence per CU.  With more sequences: 256 threads per sequence
+  // and no reservation, so that several share a CU.
+  static const size_t spread_fused = spread_lds(seq_kernel<DT, VEC, true, kSeqThreadsWide>);
+  static const size_t spread_plain = spread_lds(seq_kernel<DT, VEC, false, kSeqThreadsWide>);
   int dev = 0, ncu = 0;
   const bool few = hipGetDevice(&dev) == hipSuccess &&
                    hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
                    a.B <= ncu;
   (void)hipGetLastError();
-  const dim3 grid(unsigned(a.B)), block(kSeqThreads);
-  if (a.signal)
-    seq_kernel<DT, VEC, true><<<grid, block, few ? spread_fused : 0, a.stream>>>(P, S);
-  else
-    seq_kernel<DT, VEC, false><<<grid, block, few ? spread_plain : 0, a.stream>>>(P, S);
+  const dim3 grid(unsigned(a.B));
+  if (few) {
+    const dim3 block(kSeqThreadsWide);
+    if (a.signal)
+      seq_kernel<DT, VEC, true, kSeqThreadsWide><<<grid, block, spread_fused, a.stream>>>(P, S);
+    else
+      seq_kernel<DT, VEC, false, kSeqThreadsWide><<<grid, block, spread_plain, a.stream>>>(P, S);
+  } else {
+    const dim3 block(kSeqThreadsNarrow);
+    if (a.signal)
+      seq_kernel<DT, VEC, true, kSeqThreadsNarrow><<<grid, block, 0, a.stream>>>(P, S);
+    else
+      seq_kernel<DT, VEC, false, kSeqThreadsNarrow><<<grid, block, 0, a.stream>>>(P, S);
+  }
 }
 
 int launch_verify(const VerifyArgs &a) {
