@@ -54,6 +54,9 @@
  *     ids in ascending order and returns the smallest id whose cumulative
  *     weight exceeds u' * Z.
  *   - SL_next = clamp(floor(min(SL_hat, SL_cap) + 1/2), ceil(sl_min), sl_hi).
+ *     The paper gives no rounding rule and no worked example, so this integer
+ *     step is parity unpinned: the tests pin it to the reading above only
+ *     (SL_hat and the cap themselves are pinned by closed forms).
  *
  * Ties: a decision that sits within 1e-6 of its threshold is flagged, not
  * resolved: |u - min(1, r)| <= 1e-6 for an acceptance test, and
