@@ -72,9 +72,33 @@ __global__ __launch_bounds__(1024) void setup_kernel(int32_t B, int64_t N, int32
 // row statistics of every drafted pair
 // ---------------------------------------------------------------------------
 
-// Chunk sums of one workgroup -> one PairChunk (fixed order: lanes, then waves in fp64).
+// Greedy pairs: each wavefront's smallest token id holding the chunk maximum
+// M of the target row, into red[wave] (0xffffffff if none).  A thread's slots
+// ascend in token order in every layout, so its first slot equal to M is its
+// smallest such token.  `z(i)` is slot i of this thread's logits.
+template <int DT, bool VEC, typename Z>
+__device__ __forceinline__ void wave_chunk_argmax(float M, Z z, int64_t chunk, uint32_t *red) {
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  int first = -1;
+#pragma unroll
+  for (int i = kEltsPerThread - 1; i >= 0; --i)
+    if (z(i) == M) first = i;
+  uint32_t best = first >= 0 ? uint32_t(Layout<DT, VEC>::index(chunk, first, t)) : 0xffffffffu;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t y = __shfl_xor(best, o);
+    best = y < best ? y : best;
+  }
+  if (lane == 0) red[wave] = best;
+}
+
+// Chunk sums of one workgroup -> one PairChunk (fixed order: lanes, then waves
+// in fp64); with `arg` set (greedy pairs), also the chunk maximum M of the
+// target row and the smallest token holding it, from the per-wave candidates
+// wave_chunk_argmax left in red_arg (the same barrier serves both).
 __device__ __forceinline__ void write_pair_chunk(float rt, float rd, float sp, float sq, float a, float h,
-                                                 float (*red)[kWaves], PairChunk *out) {
+                                                 float (*red)[kWaves], PairChunk *out, float M,
+                                                 const uint32_t *red_arg, ChunkArg *arg) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   sp = wave_sum(sp);
   sq = wave_sum(sq);
@@ -100,33 +124,12 @@ __device__ __forceinline__ void write_pair_chunk(float rt, float rd, float sp, f
       pc.h += double(red[5][w]);
     }
     *out = pc;
-  }
-}
-
-// Greedy pairs: the chunk maximum M of the target row and the smallest token
-// id of the chunk holding it, written to *out (one per chunk).  `z(i)` is slot
-// i of this thread's logits.
-template <int DT, bool VEC, typename Z>
-__device__ __forceinline__ void write_chunk_argmax(float M, Z z, int64_t chunk, ChunkArg *out, uint32_t *red) {
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  uint32_t best = 0xffffffffu;
+    if (arg) {
+      uint32_t m = red_arg[0];
 #pragma unroll
-  for (int i = 0; i < kEltsPerThread; ++i) {
-    const uint32_t idx = uint32_t(Layout<DT, VEC>::index(chunk, i, t));
-    if (z(i) == M && idx < best) best = idx;
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint32_t y = __shfl_xor(best, o);
-    best = y < best ? y : best;
-  }
-  if (lane == 0) red[wave] = best;
-  __syncthreads();
-  if (t == 0) {
-    uint32_t m = red[0];
-#pragma unroll
-    for (int v = 1; v < kWaves; ++v) m = red[v] < m ? red[v] : m;
-    *out = ChunkArg{M, int32_t(m)};
+      for (int v = 1; v < kWaves; ++v) m = red_arg[v] < m ? red_arg[v] : m;
+      *arg = ChunkArg{M, int32_t(m)};
+    }
   }
 }
 
@@ -156,9 +159,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
   // chunk maxima -> the reference shifts every exponential of the chunk uses
   const float Mt = block_max(raw_max(rt_), red[0]);
   const float Md = block_max(raw_max(rd_), red[1]);
-  if (greedy)
-    write_chunk_argmax<DSDE_BF16, true>(Mt, [&](int i) { return pick_bf16(rt_, i); }, chunk,
-                                        chunk_arg + int64_t(w.slot) * nc + chunk, red_arg);
+  if (greedy) wave_chunk_argmax<DSDE_BF16, true>(Mt, [&](int i) { return pick_bf16(rt_, i); }, chunk, red_arg);
   const float rt = Mt * c, rd = Md * c;
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   acc_vec(rt_.v0, rd_.v0, c, rt, rd, s);
@@ -186,7 +187,8 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
     }
   }
   write_pair_chunk(rt, rd, s[0] + s[4], s[1] + s[5], s[2] + s[6], s[3] + s[7], red,
-                   out + int64_t(w.slot) * nc + chunk);
+                   out + int64_t(w.slot) * nc + chunk, Mt, red_arg,
+                   greedy ? chunk_arg + int64_t(w.slot) * nc + chunk : nullptr);
 }
 
 // fp32 rows, or rows without 16-byte alignment.
@@ -222,9 +224,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
   }
   const float Mt = block_max(mt, red[0]);
   const float Md = block_max(md, red[1]);
-  if (greedy)
-    write_chunk_argmax<DT, VEC>(Mt, [&](int i) { return zt[i]; }, chunk, chunk_arg + int64_t(w.slot) * nc + chunk,
-                                red_arg);
+  if (greedy) wave_chunk_argmax<DT, VEC>(Mt, [&](int i) { return zt[i]; }, chunk, red_arg);
   const float rt = Mt * c, rd = Md * c;
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -249,7 +249,8 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
     }
   }
   write_pair_chunk(rt, rd, s[0] + s[4], s[1] + s[5], s[2] + s[6], s[3] + s[7], red,
-                   out + int64_t(w.slot) * nc + chunk);
+                   out + int64_t(w.slot) * nc + chunk, Mt, red_arg,
+                   greedy ? chunk_arg + int64_t(w.slot) * nc + chunk : nullptr);
 }
 
 }  // namespace
