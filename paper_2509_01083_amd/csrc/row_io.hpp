@@ -112,6 +112,32 @@ struct RawBf16 {
   uint4 v0, v1, v2, v3;
 };
 
+// The same loads without the padding (indices clamped into the row), and the
+// padding applied afterwards: callers that issue many loads up front pad only
+// where the values are used, so that no load waits for another.
+__device__ __forceinline__ RawBf16 issue_raw_bf16(const void *row, int64_t V, int64_t chunk, int t) {
+  const uint4 *p = (const uint4 *)row;
+  const int64_t last = V / 8 - 1;
+  const int64_t i0 = chunk * 1024 + t;
+  RawBf16 r;
+  r.v0 = stream_load(p + min(i0, last));
+  r.v1 = stream_load(p + min(i0 + 256, last));
+  r.v2 = stream_load(p + min(i0 + 512, last));
+  r.v3 = stream_load(p + min(i0 + 768, last));
+  return r;
+}
+__device__ __forceinline__ RawBf16 pad_raw_bf16(const RawBf16 &a, int64_t V, int64_t chunk, int t) {
+  const int64_t last = V / 8 - 1;
+  const int64_t i0 = chunk * 1024 + t;
+  const uint4 pad = make_uint4(kPadBf16x2, kPadBf16x2, kPadBf16x2, kPadBf16x2);
+  RawBf16 r;
+  r.v0 = i0 <= last ? a.v0 : pad;
+  r.v1 = i0 + 256 <= last ? a.v1 : pad;
+  r.v2 = i0 + 512 <= last ? a.v2 : pad;
+  r.v3 = i0 + 768 <= last ? a.v3 : pad;
+  return r;
+}
+
 __device__ __forceinline__ RawBf16 load_raw_bf16(const void *row, int64_t V, int64_t chunk, int t) {
   const uint4 *p = (const uint4 *)row;
   const int64_t last = V / 8 - 1;

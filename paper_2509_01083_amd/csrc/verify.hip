@@ -179,6 +179,33 @@ __device__ inline double residual_chunk(const char *trow, const char *drow, int6
                                         const DrawJob &job) {
   const int lane = threadIdx.x & 63;
   float sw[kVirt];
+  if constexpr (DT == DSDE_BF16 && VEC) {
+    // every load of the chunk (both rows, all four chunk-layout threads: 32 KiB
+    // per wavefront) is issued before any value is used, then the same sums in
+    // the same order as below
+    RawBf16 rt[kVirt], rd[kVirt];
+#pragma unroll
+    for (int k = 0; k < kVirt; ++k) {
+      rt[k] = issue_raw_bf16(trow, V, ch, lane + 64 * k);
+      rd[k] = issue_raw_bf16(drow, V, ch, lane + 64 * k);
+    }
+#pragma unroll
+    for (int k = 0; k < kVirt; ++k) {
+      const RawBf16 t_ = pad_raw_bf16(rt[k], V, ch, lane + 64 * k), d_ = pad_raw_bf16(rd[k], V, ch, lane + 64 * k);
+      float a = 0.f;
+#pragma unroll
+      for (int i = 0; i < kEltsPerThread; ++i) {
+        const float p = fast_exp2(fmaf(pick_bf16(t_, i), job.scale, -job.mt)) * job.inv_sp;
+        const float q = fast_exp2(fmaf(pick_bf16(d_, i), job.scale, -job.md)) * job.inv_sq;
+        a += fmaxf(p - q, 0.0f);
+      }
+      sw[k] = wave_sum(a);
+    }
+    double w = 0.0;
+#pragma unroll
+    for (int k = 0; k < kVirt; ++k) w += double(sw[k]);
+    return w;
+  }
 #pragma unroll kVirtUnroll<DT, VEC>
   for (int k = 0; k < kVirt; ++k) {
     float zt[kEltsPerThread], zd[kEltsPerThread];
