@@ -160,26 +160,34 @@ def main():
     }
 
     # streaming-read ceiling of this GPU: the library's read-reduce probe over
-    # 4 GiB (16x the last-level cache), timed with the same fence-free events
+    # 4 GiB (16x the last-level cache), and over as many bytes as one launch of
+    # the statistics kernel reads (the same launch-size ramp-up and tail), each
+    # timed with the same fence-free events
     if not args.no_stream_ceiling:
-        buf = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
-        acc = torch.empty((4 << 30) // 32768, dtype=torch.int32, device=dev)
-        for _ in range(2):
-            dsde.stream_read(buf, acc)
-        e0, e1 = HipEvent(), HipEvent()
-        reps = 10
-        torch.cuda.synchronize()
-        _record(e0, stream)
-        for _ in range(reps):
-            dsde.stream_read(buf, acc)
-        _record(e1, stream)
-        torch.cuda.synchronize()
-        ceil_gbps = reps * buf.numel() / (e0.elapsed_ms(e1) * 1e-3) / 1e9
-        e0.destroy()
-        e1.destroy()
-        del buf
-        result["stream_read_ceiling"] = {"gbps": ceil_gbps, "bytes": 4 << 30, "launches": reps}
+        def probe(nbytes, reps):
+            buf = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+            acc = torch.empty(-(-nbytes // 32768), dtype=torch.int32, device=dev)
+            for _ in range(2):
+                dsde.stream_read(buf, acc)
+            e0, e1 = HipEvent(), HipEvent()
+            torch.cuda.synchronize()
+            _record(e0, stream)
+            for _ in range(reps):
+                dsde.stream_read(buf, acc)
+            _record(e1, stream)
+            torch.cuda.synchronize()
+            gbps = reps * nbytes / (e0.elapsed_ms(e1) * 1e-3) / 1e9
+            e0.destroy()
+            e1.destroy()
+            del buf, acc
+            return gbps
+        ceil_gbps = probe(4 << 30, 10)
+        same = k1_bytes // 32768 * 32768
+        same_gbps = probe(same, 50)
+        result["stream_read_ceiling"] = {"gbps": ceil_gbps, "bytes": 4 << 30, "launches": 10,
+                                         "same_bytes_gbps": same_gbps, "same_bytes": same, "same_launches": 50}
         result["roofline"]["frac_of_stream_ceiling"] = k1_gbps / ceil_gbps
+        result["roofline"]["frac_of_same_bytes_read"] = k1_gbps / same_gbps
 
     result["straggler"] = straggler_report(outs[last], k_max)
 
