@@ -82,16 +82,19 @@ def test_large_vocab(gpu_lib, V, dtype):
     check_step(gpu_lib, step, f"large vocab V={V} {dtype}")
 
 
-def test_large_batch(gpu_lib):
-    """More sequences than the set-up kernel has threads (its looping path),
-    ragged SL including 0, mixed temperatures and greedy sequences."""
-    rng = np.random.default_rng(1500)
-    B, V = 1500, 300
+@pytest.mark.parametrize("V,dtype", [(300, "bf16"), (512, "bf16"), (512, "fp32"), (301, "fp32")])
+def test_large_batch(gpu_lib, V, dtype):
+    """More sequences than CUs and than the set-up kernel has threads (the
+    256-thread per-sequence kernel and the set-up's looping path), ragged SL
+    including 0, mixed temperatures and greedy sequences; vectorised (V a
+    multiple of the vector width) and scalar row paths."""
+    rng = np.random.default_rng(1500 + V)
+    B = 1500
     sls = rng.integers(0, 4, B).tolist()
     target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V, noise=0.8)
     temps = rng.choice([0.0, 0.7, 1.0, 1.3], B).tolist()
-    step = step_from_arrays(target, draft, sls, tokens, temps, u_acc, u_res, 3)
-    _, _, rep = check_step(gpu_lib, step, f"large batch B={B}")
+    step = step_from_arrays(target, draft, sls, tokens, temps, u_acc, u_res, 3, dtype)
+    _, _, rep = check_step(gpu_lib, step, f"large batch B={B} V={V} {dtype}")
     assert rep["compared"] >= 0.9 * B
 
 
