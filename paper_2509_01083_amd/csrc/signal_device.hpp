@@ -6,14 +6,11 @@
 #include <math.h>
 
 #include "common.hpp"
+#include "lanes.hpp"
 
 namespace dsde {
 
-__device__ __forceinline__ double wave_sum_f64(double v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
+__device__ __forceinline__ double wave_sum_f64(double v) { return lanes::wave_sum(v); }
 
 // Ring slots one wavefront keeps in registers: with W <= 64 * kRingRegs every
 // window entry is read from registers, larger rings are read from memory.
@@ -259,8 +256,7 @@ __device__ inline void block_next_sl(int32_t B, const float *sf, const float *wv
     }
   }
   part = wave_sum_f64(part);
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
+  cnt = lanes::wave_sum(cnt);
   if (lane == 0) {
     red_s[wave] = part;
     red_n[wave] = cnt;

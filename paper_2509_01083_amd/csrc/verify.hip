@@ -71,18 +71,14 @@ struct DrawJob {
   int32_t token;         // greedy: the emitted token when it is already known
 };
 
-// xor-butterfly reductions inside aligned groups of G lanes (G a power of two)
+// reductions inside aligned groups of G lanes (G = 16, 32 or 64)
 template <int G>
 __device__ __forceinline__ float group_max(float v) {
-#pragma unroll
-  for (int o = G / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  return lanes::group_reduce<G>(v, lanes::Max{});
 }
 template <int G>
 __device__ __forceinline__ double group_sum(double v) {
-#pragma unroll
-  for (int o = G / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  return lanes::group_reduce<G>(v, lanes::Add{});
 }
 
 // Combines the chunk partials of every drafted pair of one sequence (stored
@@ -154,8 +150,7 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
     if (chunk_arg) {  // the row argmax: smallest token among the chunks holding the row maximum
       const float zm = group_max<G>(lz);
       arg = larg != 0x7fffffff && lz == zm ? larg : 0x7fffffff;
-#pragma unroll
-      for (int o = G / 2; o > 0; o >>= 1) arg = min(arg, __shfl_xor(arg, o));
+      arg = lanes::group_reduce<G>(arg, lanes::Min{});
     }
     if (j < s && g == 0) {
       st_mt[j] = mt;
@@ -349,11 +344,7 @@ __device__ inline void bonus_argmax_chunk(const char *trow, int64_t V, int64_t c
             best = idx < best ? idx : best;
           }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const uint32_t y = __shfl_xor(best, o);
-      best = y < best ? y : best;
-    }
+    best = lanes::wave_min(best);
     *zmax_out = M;
     *idx_out = int32_t(best);
     *bad_out = __ballot(m == INFINITY || lo == -INFINITY || sum != sum) != 0;
@@ -378,11 +369,7 @@ __device__ inline void bonus_argmax_chunk(const char *trow, int64_t V, int64_t c
     }
     const float M = wave_max(m);
     uint32_t cand = m == M ? best : 0xffffffffu;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const uint32_t y = __shfl_xor(cand, o);
-      cand = y < cand ? y : cand;
-    }
+    cand = lanes::wave_min(cand);
     *zmax_out = M;
     *idx_out = int32_t(cand);
     *bad_out = __ballot(bad) != 0;
@@ -506,9 +493,7 @@ __global__ __launch_bounds__(NT) void seq_kernel(const StepParams P, const Signa
         if (!(T >= kMinTemp && T <= kMaxTemp)) e |= DSDE_ERR_TEMP;
         if (!(ur >= 0.0f && ur < 1.0f)) e |= DSDE_ERR_UNIFORM;
       }
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) e |= __shfl_xor(e, o);
-      err |= e;
+      err |= lanes::wave_or(e);
     }
     const float c = greedy ? kLog2e : kLog2e / T;  // the same values as the set-up's scale
     const bool active = lane < s && !err;
@@ -668,12 +653,10 @@ __global__ __launch_bounds__(NT) void seq_kernel(const StepParams P, const Signa
           bch = ch;
         }
       }
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) bad |= __shfl_xor(bad, o);
+      bad = lanes::wave_or(bad);
       const float M = wave_max(best);
       int32_t cand = bch != 0x7fffffff && best == M ? bch : 0x7fffffff;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) cand = min(cand, __shfl_xor(cand, o));
+      cand = lanes::wave_min(cand);
       if (bad) {
         // a NaN or infinite logit in the bonus row: no token is emitted
         if (lane < width) tok[lane] = P.pad_id;
@@ -699,8 +682,7 @@ __global__ __launch_bounds__(NT) void seq_kernel(const StepParams P, const Signa
         ref_max = fmaxf(ref_max, ch_ref[ch]);
       }
       ref_max = wave_max(ref_max);
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) bad |= __shfl_xor(bad, o);
+      bad = lanes::wave_or(bad);
     }
     auto weight = [&](int32_t ch, int m) -> double {
       return m == 0 ? ch_w[ch] : m == 1 ? ch_p[ch] : ch_w[ch] * exp2(double(ch_ref[ch]) - double(ref_max));
@@ -726,22 +708,16 @@ __global__ __launch_bounds__(NT) void seq_kernel(const StepParams P, const Signa
       for (int32_t c0 = 0; c0 < nc; c0 += 64) {
         const int32_t ch = c0 + lane;
         const double w = ch < nc ? weight(ch, mode) : 0.0;
-        double incl = w;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const double y = __shfl_up(incl, o);
-          if (lane >= o) incl += y;
-        }
-        incl = base + incl;
-        double excl = __shfl_up(incl, 1);
-        if (lane == 0) excl = base;
+        const lanes::Scan<double> sc = lanes::wave_scan(w);
+        const double incl = base + sc.incl;
+        const double excl = lane == 0 ? base : base + sc.excl;
         const uint64_t cand = __ballot(ch < nc && w > 0.0 && excl <= target_mass);
         if (cand) {
           const int l = 63 - __builtin_clzll(cand);
           best = c0 + l;
-          best_excl = __shfl(excl, l);
+          best_excl = lanes::readlane(excl, l);
         }
-        base = __shfl(incl, 63);
+        base = lanes::readlane(incl, 63);
       }
       if (lane == 0) {
         const int32_t chunk = best >= 0 ? best : 0;
@@ -815,19 +791,12 @@ __global__ __launch_bounds__(NT) void seq_kernel(const StepParams P, const Signa
     run_total += double(w[i]);
     if (w[i] > 0.0f) last = i;
   }
-  double incl = run_total;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const double y = __shfl_up(incl, o);
-    if (lane >= o) incl += y;
-  }
-  if (lane == 63) s_wave_total[wave] = incl;
+  const lanes::Scan<double> sc = lanes::wave_scan(run_total);
+  if (lane == 63) s_wave_total[wave] = sc.incl;
   __syncthreads();
   double base = 0.0;
   for (int v = 0; v < wave; ++v) base += s_wave_total[v];
-  incl = base + incl;
-  double excl = __shfl_up(incl, 1);
-  if (lane == 0) excl = base;
+  const double excl = lane == 0 ? base : base + sc.excl;
   // the thread holding the target: the last one with positive weight whose
   // exclusive prefix is <= the target (rounding past the chunk's total lands
   // on its last positive weight)
