@@ -22,6 +22,7 @@ constexpr int kQuadSwap2 = 0x4E;       // quad_perm [2,3,0,1]: lane i reads lane
 constexpr int kRowHalfMirror = 0x141;  // lane i reads lane 7 - i of its group of 8
 constexpr int kRowMirror = 0x140;      // lane i reads lane 15 - i of its row
 constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;  // i reads i - n (row)
+constexpr int kRowRor4 = 0x124, kRowRor8 = 0x128;  // i reads (i - n) mod 16 (row rotation)
 
 // A DPP move of 32 bits; lanes whose source lies outside the row read 0.
 template <int CTRL>
@@ -100,6 +101,35 @@ __device__ __forceinline__ T group_reduce(T v, OP op) {
 
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) { return group_reduce<64>(v, Add{}); }
+
+// Sixteen sums at once (a reduce-scatter): on return lane i of each row of 16
+// holds the sum over the 16 lanes of its row of a[i % 16].  Each step halves
+// the entries a lane keeps and adds the partner's copy of the kept half:
+// partners differ in lane bit 0, 1, 2, 3 in turn (a rotation by 4 or 8 pairs
+// lanes that agree in the bits already used and differ in the next one), so
+// 15 DPP additions do the work of 16 row sums.
+__device__ __forceinline__ float row_transpose_sum16(const float (&a)[16]) {
+  const int l = threadIdx.x & 15;
+  const bool b0 = l & 1, b1 = l & 2, b2 = l & 4, b3 = l & 8;
+  float s8[8], s4[4], s2[2];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {  // entry 2i + b0
+    const float keep = b0 ? a[2 * i + 1] : a[2 * i], send = b0 ? a[2 * i] : a[2 * i + 1];
+    s8[i] = keep + dpp<kQuadSwap1>(send);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {  // entry 4i + 2 b1 + b0
+    const float keep = b1 ? s8[2 * i + 1] : s8[2 * i], send = b1 ? s8[2 * i] : s8[2 * i + 1];
+    s4[i] = keep + dpp<kQuadSwap2>(send);
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {  // entry 8i + 4 b2 + 2 b1 + b0
+    const float keep = b2 ? s4[2 * i + 1] : s4[2 * i], send = b2 ? s4[2 * i] : s4[2 * i + 1];
+    s2[i] = keep + dpp<kRowRor4>(send);
+  }
+  const float keep = b3 ? s2[1] : s2[0], send = b3 ? s2[0] : s2[1];
+  return keep + dpp<kRowRor8>(send);
+}
 __device__ __forceinline__ float wave_max(float v) { return group_reduce<64>(v, Max{}); }
 template <typename T>
 __device__ __forceinline__ T wave_min(T v) { return group_reduce<64>(v, Min{}); }
