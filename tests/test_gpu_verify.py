@@ -249,6 +249,49 @@ def test_constructed_ties(gpu_lib):
     assert rep["acc_ties"] >= 24 and rep["cdf_ties"] >= 24, rep
 
 
+@pytest.mark.parametrize("V,dtype", [(3 * 8192 + 704, "bf16"), (3 * 8192 + 704, "fp32"), (3 * 8192 + 705, "bf16"),
+                                     (3 * 8192 + 705, "fp32")])
+def test_draw_at_sub_block_and_chunk_boundaries(gpu_lib, V, dtype):
+    """The draw's three levels (chunk of 8192, sub-block of 512, element) at
+    their edges: all mass on tokens that open or close a sub-block or a chunk,
+    up to the last token of a partial last chunk, and u' in the middle of each
+    token's CDF interval.  Every sequence rejects its one draft (q is one-hot on
+    a token p does not hold) or accepts it and draws from the bonus row, so the
+    residual and the bonus draws are both checked, against the oracle and
+    against the token the construction fixes.  V = 8k + 704 takes the
+    vectorised paths, V = 8k + 705 the scalar ones."""
+    hot = np.array([0, 511, 512, 1023, 4095, 8191, 8192, 8703, 16383, 16384, 24575, 24576, V - 1])
+    H = len(hot)
+    B = 2 * H
+    sls = [1] * B
+    rng = np.random.default_rng(V)
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V)
+    other = 3000  # not a hot token
+    for b in range(B):
+        i = b % H
+        row = np.full(V, -30.0, np.float32)
+        row[hot] = 0.0
+        if b < H:  # reject: q one-hot on `other`, p spread evenly over the hot tokens
+            target[2 * b] = row
+            draft[b] = -30.0
+            draft[b, other] = 30.0
+            tokens[b] = other
+            u_acc[b] = 0.5
+        else:      # accept (equal rows), then the bonus row holds the hot tokens
+            draft[b] = target[2 * b]
+            tokens[b] = other
+            u_acc[b] = 0.0
+            target[2 * b + 1] = row
+        u_res[b] = (i + 0.5) / H
+    step = step_from_arrays(target, draft, sls, tokens, [1.0] * B, u_acc, u_res, 1, dtype)
+    got, ref, rep = check_step(gpu_lib, step, f"draw at boundaries V={V} {dtype}")
+    assert rep["compared"] == B, rep
+    want = np.concatenate([hot, hot])
+    assert (got["accepted"] == np.array([0] * H + [1] * H)).all()
+    drawn = got["tokens"][np.arange(B), got["accepted"]]
+    assert (drawn == want).all(), (drawn, want)
+
+
 @pytest.mark.parametrize("V,dtype", [(5000, "bf16"), (5000, "fp32"), (8200, "bf16"), (600000, "bf16")])
 def test_greedy_ties_and_emissions(gpu_lib, V, dtype):
     """Greedy verification (T = 0) with repeated maxima inside and across
