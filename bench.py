@@ -352,6 +352,17 @@ class HipEvent:
         HipEvent._hip.hipEventDestroy(self.handle)
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(step, out, st, seconds):
     """The oracle, as it stands, on the host: whole steps (verify, signal update,
     SL rule) repeated until about ``seconds`` of CPU time have passed; also checks
@@ -378,6 +389,11 @@ def cpu_baseline(step, out, st, seconds):
             break
     dt = (time.perf_counter() - t0) / n
     rows = 2 * int(host["cu_sl"][-1]) + len(host["sl"])
+    # one more step of the oracle's verify on a single thread (the signal update
+    # and SL rule are a few microseconds), for the per-core rate
+    t1 = time.perf_counter()
+    oracle.verify(**host, n_threads=1)
+    dt1 = time.perf_counter() - t1
     # parity of the timed GPU step against the oracle (ties excluded)
     acc = out["accepted"].cpu().numpy()
     tok = out["tokens"].cpu().numpy()
@@ -389,7 +405,8 @@ def cpu_baseline(step, out, st, seconds):
     cpu = {"value": rows / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
            "sample": f"the full step (verify + signal + SL rule; B={len(host['sl'])}, {rows} logit rows, "
                      f"V={host['V']}), {n} repetition(s), {threads} threads, fp64",
-           "seconds_per_step": dt}
+           "seconds_per_step": dt, "cpu_model": cpu_model(),
+           "single_thread": {"value": rows / dt1, "unit": "rows/s", "seconds_per_step": dt1}}
     parity = {"compared": int(ok.sum()), "ties": int((ref["acc_tie"] | ref["cdf_tie"]).sum()),
               "mismatches": mism, "kld_err_over_tolerance": kerr}
     return cpu, parity
