@@ -242,6 +242,141 @@ int32_t dsde_calibrate_sl_max(int32_t B, const int32_t *a_max, const double *kld
                               const float *kld_max, float eps, int32_t pooled, float *sl_max, void *stream);
 
 /*
+ * Vocabulary-sharded verification, for logits that arrive split by vocabulary,
+ * as a tensor-parallel LM head produces them when the target model spans
+ * several GPUs (the paper's experiments run on one eight-GPU server, Sec. 4.1;
+ * how the model is split there is not stated).  Shard g of G holds, for every row
+ * of the packed layout above, the logits of one contiguous vocabulary slice
+ * [v_begin_g, v_begin_g + V_g), as row-major [rows, V_g] arrays; the slices of
+ * g = 0, 1, ..., G-1 tile [0, V) in ascending order.  A step is four calls on
+ * every shard with two exchanges between them, which the caller makes (an
+ * all-gather across the G GPUs, e.g. over RCCL):
+ *
+ *   1. dsde_shard_stats      this slice's statistics of every drafted pair:
+ *                            part [N]                   -> gather parts [G][N]
+ *   2. dsde_shard_accept     from parts: KLD, acceptance, the accepted drafts
+ *                            and each sequence's draw job, jobs [B] (every
+ *                            shard computes the same values)
+ *   3. dsde_shard_draw_mass  this slice's share of each sequence's draw
+ *                            weight: mass [B]           -> gather masses [G][B]
+ *   4. dsde_shard_draw_pick  the emitted token: drawn[b] >= 0 on the shard
+ *                            that determines it (the one whose slice holds
+ *                            the inverse-CDF point, or every shard for greedy
+ *                            rows), -1 elsewhere, so an all-reduce max gives
+ *                            it to every shard; that shard also writes it into
+ *                            tokens.
+ *
+ * The exchanges carry 64 bytes per drafted position and 32 bytes per sequence
+ * from each shard.  Results are those of dsde_verify on the whole rows, with
+ * the sums split at slice boundaries: accepted counts, tokens and error bits
+ * outside the tie bands, KLD within the same tolerance.  dsde_kld_signal and
+ * dsde_next_sl then run unchanged on every shard (their inputs are identical
+ * there).  Every pointer, layout and error rule of dsde_verify applies; the
+ * calls of one shard share its workspace (dsde_shard_workspace_bytes), whose
+ * contents pass from call 1 to 2 (none), 3 to 4 (the slice's chunk totals).
+ */
+typedef struct {
+  float mt, md;      /* the slice's largest z c of the target and the draft row (log2 domain) */
+  double sp, sq;     /* sum over the slice of 2^(z_t c - mt), of 2^(z_d c - md) */
+  double a;          /* sum of 2^(z_t c - mt) ((z_t c - mt) - (z_d c - md)) */
+  double h;          /* sum of 2^(z_d c - md) (z_d c - md) */
+  float zt, zd;      /* target and draft logit at the drafted token, when the slice holds it */
+  int32_t has_token; /* 1 when the drafted token lies in the slice */
+  float zmax;        /* greedy rows (T_b = 0): the slice's largest target logit, */
+  int32_t argmax;    /* and the smallest (global) token id holding it */
+  int32_t bad;       /* 1: a NaN or infinite logit in the slice of either row */
+} dsde_shard_partial; /* 64 bytes */
+
+typedef struct {
+  int32_t kind;      /* 0: residual of the first rejected pair, 1: bonus row, 2: greedy, token
+                        known, 3: greedy, argmax of the bonus row, -1: nothing (flagged) */
+  int32_t accepted;  /* a_b */
+  int32_t target_row, draft_row; /* rows of the draw in the packed layout (draft_row -1: none) */
+  float scale;       /* log2(e) / T_b */
+  float mt, md;      /* kind 0: the whole rows' largest z c (target, draft) */
+  float inv_sp, inv_sq; /* kind 0: 1 / their sums of 2^(z c - m) */
+  float u;           /* u_res[b] */
+  int32_t token;     /* kind 2: the emitted token */
+} dsde_draw_job;     /* 44 bytes */
+
+typedef struct {
+  double mass;       /* the slice's total draw weight: max(0, p - q) (kind 0), or 2^(z c - ref)
+                        of the bonus row (kind 1); 0 otherwise */
+  double p_mass;     /* kind 0: the slice's mass of p, for the draw's fallback to p when no
+                        slice holds residual mass */
+  float ref;         /* kind 1: the slice's largest z c of the bonus row */
+  float zmax;        /* kind 3: the slice's largest bonus-row logit, */
+  int32_t argmax;    /* and the smallest (global) token id holding it */
+  int32_t bad;       /* kinds 1 and 3: a NaN or infinite logit in the slice of the bonus row */
+} dsde_shard_mass;   /* 32 bytes */
+
+/* Workspace bytes of one shard's four calls: B sequences, N drafted positions,
+ * slice width V_shard, bound k_max; 0 when the sizes are invalid. */
+size_t dsde_shard_workspace_bytes(int32_t B, int64_t N, int64_t V_shard, int32_t k_max);
+
+/*
+ * Call 1: the slice statistics of every drafted pair.
+ *   target_logits [N+B, V_shard], draft_logits [N, V_shard]   this shard's slices
+ *   v_begin, V                  the slice's first token id and the whole vocabulary
+ *                               (0 <= v_begin, 1 <= V_shard, v_begin + V_shard <= V <= DSDE_MAX_VOCAB)
+ *   sl, cu_sl, draft_tokens (global ids), temperature, B, N, k_max   as in dsde_verify
+ *   part [N]                    output, one per drafted position
+ *   seq_err [B]                 output: DSDE_ERR_LAYOUT or 0 (the layout check of dsde_verify)
+ */
+int32_t dsde_shard_stats(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V_shard,
+                         int64_t v_begin, int64_t V, int32_t B, int64_t N, int32_t k_max, const int32_t *sl,
+                         const int32_t *cu_sl, const int32_t *draft_tokens, const float *temperature,
+                         dsde_shard_partial *part, uint32_t *seq_err, void *workspace, size_t workspace_bytes,
+                         void *stream);
+
+/*
+ * Call 2: acceptance and KLD from every shard's partials.
+ *   G, parts [G][N]             the gathered partials in shard order (1 <= G <= 1024)
+ *   V                           the whole vocabulary
+ *   sl ... pad_id               as in dsde_verify
+ *   accepted, tokens, kld, row_lse, draft_entropy   as in dsde_verify, except that the
+ *                               drawn token is left to call 4 (greedy rows whose token is
+ *                               known here get it now)
+ *   jobs [B]                    output: the draw of every sequence, for calls 3 and 4
+ *   seq_err [B]                 in/out: call 1's bits, OR this call's (a drafted token
+ *                               held by no slice or by several is DSDE_ERR_TOKEN)
+ */
+int32_t dsde_shard_accept(int32_t G, const dsde_shard_partial *parts, int64_t V, int32_t B, int64_t N,
+                          int32_t k_max, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
+                          const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
+                          int32_t *accepted, int32_t *tokens, float *kld, double *row_lse, float *draft_entropy,
+                          dsde_draw_job *jobs, uint32_t *seq_err, void *stream);
+
+/*
+ * Call 3: this slice's share of each sequence's draw weight (it reads the
+ * slice of the first rejected pair, or of the bonus row, once) into mass [B];
+ * the slice's chunk totals stay in the workspace for call 4.
+ *   part [N]                    this shard's call-1 output
+ *   jobs [B]                    call 2's output
+ */
+int32_t dsde_shard_draw_mass(const void *target_logits, const void *draft_logits, int32_t dtype,
+                             int64_t V_shard, int64_t v_begin, int32_t B, int64_t N, int32_t k_max,
+                             const dsde_shard_partial *part, const dsde_draw_job *jobs, dsde_shard_mass *mass,
+                             void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Call 4: the draw.  From the gathered masses [G][B] every shard finds the
+ * slice holding u'_b Z_b (a fixed-order fp64 prefix over the slices, the rule
+ * of dsde_verify's draw); that shard scans its slice (chunk totals from call
+ * 3, the fallback to p computed here when it is needed).
+ *   g                           this shard's index (0 <= g < G)
+ *   drawn [B]                   output: the token, or -1 (see above)
+ *   accepted, tokens, seq_err   updated when a sampled bonus row holds a NaN or infinite
+ *                               logit: accepted = 0, pad_id tokens, DSDE_ERR_LOGIT (on every
+ *                               shard alike)
+ */
+int32_t dsde_shard_draw_pick(int32_t G, int32_t g, const dsde_shard_mass *masses, const void *target_logits,
+                             const void *draft_logits, int32_t dtype, int64_t V_shard, int64_t v_begin,
+                             int32_t B, int64_t N, int32_t k_max, const dsde_draw_job *jobs, int32_t pad_id,
+                             int32_t *accepted, int32_t *tokens, int32_t *drawn, uint32_t *seq_err,
+                             void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Measurement utility, not part of the method: reads `bytes` bytes of device
  * memory at `buf` with the statistics pass's access pattern (one workgroup per
  * 32 KiB, 16-byte vector loads, 1 KiB contiguous per wavefront load) and

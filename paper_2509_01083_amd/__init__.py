@@ -20,7 +20,11 @@ ERR_LAYOUT, ERR_TOKEN, ERR_LOGIT, ERR_TEMP, ERR_UNIFORM, ERR_SIGNAL, ERR_STATE =
 MAX_K = 63
 EXPORTS = ("dsde_abi_version", "dsde_status_string", "dsde_verify_workspace_bytes", "dsde_verify",
            "dsde_step", "dsde_kld_signal", "dsde_next_sl", "dsde_calibration_update", "dsde_calibrate_sl_max",
-           "dsde_set_profile_events", "dsde_stream_read")
+           "dsde_set_profile_events", "dsde_stream_read", "dsde_shard_workspace_bytes", "dsde_shard_stats",
+           "dsde_shard_accept", "dsde_shard_draw_mass", "dsde_shard_draw_pick")
+# sizes of the records the vocabulary-shard calls exchange (dsde_shard_partial,
+# dsde_draw_job, dsde_shard_mass); kept as raw bytes on the Python side
+SHARD_PARTIAL_BYTES, DRAW_JOB_BYTES, SHARD_MASS_BYTES = 64, 44, 32
 
 _lib = None
 
@@ -63,6 +67,17 @@ def load(path: str = LIB_PATH):
     lib.dsde_set_profile_events.argtypes = [P, P]
     lib.dsde_stream_read.restype = i32
     lib.dsde_stream_read.argtypes = [P, i64, P, P]
+    lib.dsde_shard_workspace_bytes.restype = sz
+    lib.dsde_shard_workspace_bytes.argtypes = [i32, i64, i64, i32]
+    lib.dsde_shard_stats.restype = i32
+    lib.dsde_shard_stats.argtypes = [P, P, i32, i64, i64, i64, i32, i64, i32, P, P, P, P, P, P, P, sz, P]
+    lib.dsde_shard_accept.restype = i32
+    lib.dsde_shard_accept.argtypes = [i32, P, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P, P, P, P, P]
+    lib.dsde_shard_draw_mass.restype = i32
+    lib.dsde_shard_draw_mass.argtypes = [P, P, i32, i64, i64, i32, i64, i32, P, P, P, P, sz, P]
+    lib.dsde_shard_draw_pick.restype = i32
+    lib.dsde_shard_draw_pick.argtypes = [i32, i32, P, P, P, i32, i64, i64, i32, i64, i32, P, i32, P, P, P, P, P,
+                                         sz, P]
     _lib = lib
     return lib
 
@@ -308,3 +323,173 @@ def stream_read(buf, out):
         raise DsdeError("stream_read: out holds fewer than one word per 32 KiB")
     _check(lib.dsde_stream_read(ctypes.c_void_p(buf.data_ptr()), nbytes, ctypes.c_void_p(out.data_ptr()),
                                 ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)))
+
+
+# ---------------------------------------------------------------------------
+# vocabulary-sharded verification (dsde_shard_*): one shard's four calls
+# ---------------------------------------------------------------------------
+
+def new_shard_workspace(B, N, V_shard, k_max, device="cuda"):
+    n = int(load().dsde_shard_workspace_bytes(B, N, V_shard, k_max))
+    if n == 0:
+        raise DsdeError("invalid sizes for the shard workspace")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def _shard_rows(target, draft, B):
+    dt = _logits_dtype(target)
+    V_shard = int(target.shape[1])
+    N = int(draft.shape[0]) if draft is not None else 0
+    if draft is not None and (draft.dtype != target.dtype or (N > 0 and int(draft.shape[1]) != V_shard)):
+        raise DsdeError("draft slice must match the target slice's dtype and width")
+    if int(target.shape[0]) != N + B:
+        raise DsdeError(f"target slice has {target.shape[0]} rows, expected N + B = {N + B}")
+    return dt, V_shard, N
+
+
+def shard_stats(target, draft, v_begin, V, sl, cu_sl, draft_tokens, temperature, k_max, workspace,
+                part=None, seq_err=None, stream=None):
+    """``dsde_shard_stats`` (call 1) on this shard's slices [rows, V_shard].  Returns
+    (part [N, 64] uint8 records, seq_err [B] int32)."""
+    lib = load()
+    B = int(sl.shape[0])
+    dt, V_shard, N = _shard_rows(target, draft, B)
+    dev = target.device
+    if part is None:
+        part = torch.empty((max(N, 1), SHARD_PARTIAL_BYTES), dtype=torch.uint8, device=dev)
+    if seq_err is None:
+        seq_err = torch.empty(B, dtype=torch.int32, device=dev)
+    rc = lib.dsde_shard_stats(
+        _ptr(target, name="target"), _ptr(draft, name="draft") if N > 0 else None, dt, V_shard, int(v_begin),
+        int(V), B, N, k_max, _ptr(sl, torch.int32, B, "sl"), _ptr(cu_sl, torch.int32, B + 1, "cu_sl"),
+        _ptr(draft_tokens, torch.int32, N, "draft_tokens") if N > 0 else None,
+        _ptr(temperature, torch.float32, B, "temperature"),
+        _ptr(part, torch.uint8, N * SHARD_PARTIAL_BYTES, "part") if N > 0 else None,
+        _ptr(seq_err, None, B, "seq_err"), _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
+        _stream(stream))
+    _check(rc)
+    return part, seq_err
+
+
+def shard_accept(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, seq_err, pad_id=-1,
+                 row_lse=None, draft_entropy=False, out=None, stream=None):
+    """``dsde_shard_accept`` (call 2) from the gathered partials parts [G, N, 64]
+    (uint8, shard order).  seq_err (call 1's) is updated in place.  Returns a dict
+    with accepted, tokens, kld, seq_err, jobs [B, 44] uint8 (and draft_entropy)."""
+    lib = load()
+    G = int(parts.shape[0])
+    B = int(sl.shape[0])
+    N = int(draft_tokens.shape[0]) if draft_tokens is not None else 0
+    dev = sl.device
+    if N > 0 and (parts.dim() != 3 or int(parts.shape[1]) < N or int(parts.shape[2]) != SHARD_PARTIAL_BYTES):
+        raise DsdeError("parts must be [G, N, 64] uint8")
+    if out is None:
+        out = {"accepted": torch.empty(B, dtype=torch.int32, device=dev),
+               "tokens": torch.empty((B, k_max + 1), dtype=torch.int32, device=dev),
+               "kld": torch.empty(max(N, 1), dtype=torch.float32, device=dev)[:N],
+               "jobs": torch.empty((B, DRAW_JOB_BYTES), dtype=torch.uint8, device=dev)}
+    out["seq_err"] = seq_err
+    if draft_entropy and "draft_entropy" not in out:
+        out["draft_entropy"] = torch.empty(max(N, 1), dtype=torch.float32, device=dev)[:N]
+    ent = out.get("draft_entropy") if draft_entropy else None
+    if N > 0 and int(parts.shape[1]) != N:
+        parts = parts[:, :N].contiguous()
+    rc = lib.dsde_shard_accept(
+        G, _ptr(parts, torch.uint8, G * N * SHARD_PARTIAL_BYTES, "parts") if N > 0 else None, int(V), B, N, k_max,
+        _ptr(sl, torch.int32, B, "sl"), _ptr(cu_sl, torch.int32, B + 1, "cu_sl"),
+        _ptr(draft_tokens, torch.int32, N, "draft_tokens") if N > 0 else None,
+        _ptr(temperature, torch.float32, B, "temperature"),
+        _ptr(u_acc, torch.float32, N, "u_acc") if N > 0 else None, _ptr(u_res, torch.float32, B, "u_res"),
+        int(pad_id), _ptr(out["accepted"], torch.int32, B, "accepted"),
+        _ptr(out["tokens"], torch.int32, B * (k_max + 1), "tokens"),
+        _ptr(out["kld"], torch.float32, N, "kld") if N > 0 else None,
+        _ptr(row_lse, torch.float64, 2 * N, "row_lse") if row_lse is not None else None,
+        _ptr(ent, torch.float32, N, "draft_entropy") if ent is not None and N > 0 else None,
+        _ptr(out["jobs"], torch.uint8, B * DRAW_JOB_BYTES, "jobs"), _ptr(seq_err, None, B, "seq_err"),
+        _stream(stream))
+    _check(rc)
+    return out
+
+
+def shard_draw_mass(target, draft, v_begin, part, jobs, k_max, workspace, mass=None, stream=None):
+    """``dsde_shard_draw_mass`` (call 3).  Returns mass [B, 32] uint8 records."""
+    lib = load()
+    B = int(jobs.shape[0])
+    dt, V_shard, N = _shard_rows(target, draft, B)
+    if mass is None:
+        mass = torch.empty((B, SHARD_MASS_BYTES), dtype=torch.uint8, device=target.device)
+    rc = lib.dsde_shard_draw_mass(
+        _ptr(target, name="target"), _ptr(draft, name="draft") if N > 0 else None, dt, V_shard, int(v_begin), B, N,
+        k_max, _ptr(part, torch.uint8, N * SHARD_PARTIAL_BYTES, "part") if N > 0 else None,
+        _ptr(jobs, torch.uint8, B * DRAW_JOB_BYTES, "jobs"), _ptr(mass, torch.uint8, B * SHARD_MASS_BYTES, "mass"),
+        _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc)
+    return mass
+
+
+def shard_draw_pick(g, masses, target, draft, v_begin, jobs, k_max, accepted, tokens, seq_err, workspace,
+                    pad_id=-1, drawn=None, stream=None):
+    """``dsde_shard_draw_pick`` (call 4) for shard g from the gathered masses
+    [G, B, 32] (uint8, shard order).  accepted, tokens and seq_err are updated in
+    place; returns drawn [B] int32 (the token where this shard determined it,
+    else -1)."""
+    lib = load()
+    G = int(masses.shape[0])
+    B = int(jobs.shape[0])
+    dt, V_shard, N = _shard_rows(target, draft, B)
+    if drawn is None:
+        drawn = torch.empty(B, dtype=torch.int32, device=target.device)
+    rc = lib.dsde_shard_draw_pick(
+        G, int(g), _ptr(masses, torch.uint8, G * B * SHARD_MASS_BYTES, "masses"), _ptr(target, name="target"),
+        _ptr(draft, name="draft") if N > 0 else None, dt, V_shard, int(v_begin), B, N, k_max,
+        _ptr(jobs, torch.uint8, B * DRAW_JOB_BYTES, "jobs"), int(pad_id),
+        _ptr(accepted, torch.int32, B, "accepted"), _ptr(tokens, torch.int32, B * (k_max + 1), "tokens"),
+        _ptr(drawn, torch.int32, B, "drawn"), _ptr(seq_err, None, B, "seq_err"),
+        _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc)
+    return drawn
+
+
+def slice_bounds(V, G):
+    """Boundaries of G near-equal contiguous vocabulary slices (multiples of 8
+    where the width allows, so that bf16 slices keep 16-byte rows)."""
+    step = -(-V // G)
+    step = -(-step // 8) * 8 if step * (G - 1) < V else step
+    bounds = [min(g * step, V) for g in range(G)] + [V]
+    return [(bounds[g], bounds[g + 1]) for g in range(G) if bounds[g + 1] > bounds[g]]
+
+
+def verify_sharded(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, slices,
+                   pad_id=-1, row_lse=None, draft_entropy=False):
+    """The four shard calls for every slice of ``slices`` ([(v_begin, v_end), ...],
+    ascending, tiling [0, V)) run on one device, the exchanges being the gathered
+    tensors themselves: the sharded path's results on one GPU, for tests and
+    measurements.  Returns the dict of dsde_verify's outputs plus ``drawn``
+    (the all-reduce max of every shard's drawn[])."""
+    V = int(target.shape[1])
+    B = int(sl.shape[0])
+    N = int(draft.shape[0]) if draft is not None else 0
+    dev = target.device
+    shards = []
+    for (v0, v1) in slices:
+        t = target[:, v0:v1].contiguous()
+        d = draft[:, v0:v1].contiguous() if N > 0 else None
+        ws = new_shard_workspace(B, N, v1 - v0, k_max, device=dev)
+        shards.append((v0, t, d, ws))
+    parts, errs = [], []
+    for (v0, t, d, ws) in shards:
+        p, e = shard_stats(t, d, v0, V, sl, cu_sl, draft_tokens, temperature, k_max, ws)
+        parts.append(p[:max(N, 1)])
+        errs.append(e)
+    seq_err = errs[0].clone()
+    out = shard_accept(torch.stack(parts), V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, seq_err,
+                       pad_id=pad_id, row_lse=row_lse, draft_entropy=draft_entropy)
+    masses = torch.stack([shard_draw_mass(t, d, v0, p, out["jobs"], k_max, ws)
+                          for (v0, t, d, ws), p in zip(shards, parts)])
+    drawn = [shard_draw_pick(g, masses, t, d, v0, out["jobs"], k_max, out["accepted"], out["tokens"], seq_err, ws,
+                             pad_id=pad_id)
+             for g, (v0, t, d, ws) in enumerate(shards)]
+    out["drawn"] = torch.stack(drawn).max(dim=0).values
+    out["shard_seq_err"] = errs
+    return out
+

@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libdsde.so")
-SOURCES = ["api.hip", "stats.hip", "verify.hip", "signal.hip", "probe.hip"]
+SOURCES = ["api.hip", "stats.hip", "verify.hip", "shard.hip", "signal.hip", "probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",

@@ -3,6 +3,7 @@
 #include <math.h>
 
 #include "common.hpp"
+#include "shard.hpp"
 
 namespace {
 
@@ -207,6 +208,105 @@ int32_t dsde_set_profile_events(void *start, void *stop) {
   g_prof_start = static_cast<hipEvent_t>(start);
   g_prof_stop = static_cast<hipEvent_t>(stop);
   return DSDE_OK;
+}
+
+size_t dsde_shard_workspace_bytes(int32_t B, int64_t N, int64_t V_shard, int32_t k_max) {
+  if (!verify_sizes_ok(B, N, V_shard, k_max)) return 0;
+  if (int64_t(B) * ((V_shard + dsde::kChunk - 1) / dsde::kChunk) * 64 >= (int64_t(1) << 31)) return 0;
+  return dsde::shard_layout(B, N, V_shard, k_max).total;
+}
+
+}  // extern "C"
+
+namespace {
+
+// The checks every shard call shares: element type, sizes, the slice inside
+// the vocabulary, and the workspace.
+int32_t shard_rows_ok(int32_t dtype, int64_t V_shard, int64_t v_begin, int64_t V, int32_t B, int64_t N,
+                      int32_t k_max, const void *target, const void *draft, void *workspace,
+                      size_t workspace_bytes) {
+  if (dtype != DSDE_FP32 && dtype != DSDE_BF16) return DSDE_INVALID_ARG;
+  if (dsde_shard_workspace_bytes(B, N, V_shard, k_max) == 0) return DSDE_INVALID_ARG;
+  if (v_begin < 0 || V < 1 || V > DSDE_MAX_VOCAB || v_begin + V_shard > V) return DSDE_INVALID_ARG;
+  if (!target || !workspace || (N > 0 && !draft)) return DSDE_INVALID_ARG;
+  if (workspace_bytes < dsde::shard_layout(B, N, V_shard, k_max).total) return DSDE_WORKSPACE_TOO_SMALL;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return DSDE_INVALID_ARG;
+  return DSDE_OK;
+}
+
+dsde::ShardRows shard_rows(const void *target, const void *draft, int32_t dtype, int64_t V_shard, int64_t v_begin,
+                           int32_t B, int64_t N, int32_t k_max, void *workspace, void *stream) {
+  dsde::ShardRows r;
+  r.target = target;
+  r.draft = draft;
+  r.dtype = dtype;
+  r.V_shard = V_shard;
+  r.v_begin = v_begin;
+  r.B = B;
+  r.N = N;
+  r.k_max = k_max;
+  r.workspace = workspace;
+  r.stream = static_cast<hipStream_t>(stream);
+  return r;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t dsde_shard_stats(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V_shard,
+                         int64_t v_begin, int64_t V, int32_t B, int64_t N, int32_t k_max, const int32_t *sl,
+                         const int32_t *cu_sl, const int32_t *draft_tokens, const float *temperature,
+                         dsde_shard_partial *part, uint32_t *seq_err, void *workspace, size_t workspace_bytes,
+                         void *stream) {
+  const int32_t st = shard_rows_ok(dtype, V_shard, v_begin, V, B, N, k_max, target_logits, draft_logits, workspace,
+                                   workspace_bytes);
+  if (st != DSDE_OK) return st;
+  if (!sl || !cu_sl || !temperature || !seq_err || (N > 0 && (!draft_tokens || !part))) return DSDE_INVALID_ARG;
+  return dsde::launch_shard_stats(
+      shard_rows(target_logits, draft_logits, dtype, V_shard, v_begin, B, N, k_max, workspace, stream), V, sl, cu_sl,
+      draft_tokens, temperature, part, seq_err);
+}
+
+int32_t dsde_shard_accept(int32_t G, const dsde_shard_partial *parts, int64_t V, int32_t B, int64_t N,
+                          int32_t k_max, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
+                          const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
+                          int32_t *accepted, int32_t *tokens, float *kld, double *row_lse, float *draft_entropy,
+                          dsde_draw_job *jobs, uint32_t *seq_err, void *stream) {
+  if (G < 1 || G > 1024 || !verify_sizes_ok(B, N, V, k_max)) return DSDE_INVALID_ARG;
+  if (!sl || !cu_sl || !temperature || !u_res || !accepted || !tokens || !jobs || !seq_err) return DSDE_INVALID_ARG;
+  if (N > 0 && (!parts || !draft_tokens || !u_acc || !kld)) return DSDE_INVALID_ARG;
+  return dsde::launch_shard_accept(G, parts, V, B, N, k_max, sl, cu_sl, draft_tokens, temperature, u_acc, u_res,
+                                   pad_id, accepted, tokens, kld, row_lse, draft_entropy, jobs, seq_err,
+                                   static_cast<hipStream_t>(stream));
+}
+
+int32_t dsde_shard_draw_mass(const void *target_logits, const void *draft_logits, int32_t dtype,
+                             int64_t V_shard, int64_t v_begin, int32_t B, int64_t N, int32_t k_max,
+                             const dsde_shard_partial *part, const dsde_draw_job *jobs, dsde_shard_mass *mass,
+                             void *workspace, size_t workspace_bytes, void *stream) {
+  const int32_t st = shard_rows_ok(dtype, V_shard, v_begin, v_begin + V_shard, B, N, k_max, target_logits,
+                                   draft_logits, workspace, workspace_bytes);
+  if (st != DSDE_OK) return st;
+  if (!jobs || !mass || (N > 0 && !part)) return DSDE_INVALID_ARG;
+  return dsde::launch_shard_draw_mass(
+      shard_rows(target_logits, draft_logits, dtype, V_shard, v_begin, B, N, k_max, workspace, stream), part, jobs,
+      mass);
+}
+
+int32_t dsde_shard_draw_pick(int32_t G, int32_t g, const dsde_shard_mass *masses, const void *target_logits,
+                             const void *draft_logits, int32_t dtype, int64_t V_shard, int64_t v_begin,
+                             int32_t B, int64_t N, int32_t k_max, const dsde_draw_job *jobs, int32_t pad_id,
+                             int32_t *accepted, int32_t *tokens, int32_t *drawn, uint32_t *seq_err,
+                             void *workspace, size_t workspace_bytes, void *stream) {
+  if (G < 1 || G > 1024 || g < 0 || g >= G) return DSDE_INVALID_ARG;
+  const int32_t st = shard_rows_ok(dtype, V_shard, v_begin, v_begin + V_shard, B, N, k_max, target_logits,
+                                   draft_logits, workspace, workspace_bytes);
+  if (st != DSDE_OK) return st;
+  if (!masses || !jobs || !accepted || !tokens || !drawn || !seq_err) return DSDE_INVALID_ARG;
+  return dsde::launch_shard_draw_pick(
+      shard_rows(target_logits, draft_logits, dtype, V_shard, v_begin, B, N, k_max, workspace, stream), G, g, masses,
+      jobs, pad_id, accepted, tokens, drawn, seq_err);
 }
 
 int32_t dsde_stream_read(const void *buf, int64_t bytes, uint32_t *out, void *stream) {

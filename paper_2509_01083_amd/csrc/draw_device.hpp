@@ -110,14 +110,35 @@ __device__ __forceinline__ double group_sum(double v) {
   return lanes::group_reduce<G>(v, lanes::Add{});
 }
 
+// Folds the statistics (mt, md, sp, sq, a, h) of one more part of a row pair
+// (a chunk, or a vocabulary slice) into a running set: both are rescaled to
+// the larger reference shifts; the KL and entropy accumulators take the shift
+// of the log-ratio along (a = sum 2^at (at - ad) with at, ad relative to the
+// references).
+__device__ __forceinline__ void fold_pair_stats(float &lmt, float &lmd, double &lsp, double &lsq, double &la,
+                                                double &lh, float qmt, float qmd, double qsp, double qsq, double qa,
+                                                double qh) {
+  const float nt = fmaxf(lmt, qmt), nd = fmaxf(lmd, qmd);
+  const double d0t = double(lmt) - nt, d0d = double(lmd) - nd;
+  const double d1t = double(qmt) - nt, d1d = double(qmd) - nd;
+  const double f0t = exp2_taylor(d0t), f0d = exp2_taylor(d0d), f1t = exp2_taylor(d1t), f1d = exp2_taylor(d1d);
+  la = f0t * (la + lsp * (d0t - d0d)) + f1t * (qa + qsp * (d1t - d1d));
+  lh = f0d * (lh + lsq * d0d) + f1d * (qh + qsq * d1d);
+  lsp = f0t * lsp + f1t * qsp;
+  lsq = f0d * lsq + f1d * qsq;
+  lmt = nt;
+  lmd = nd;
+}
+
 // Combines the chunk partials of every drafted pair of one sequence (stored
 // under slots slot0 + j): groups of G lanes, one pair per group, lane g of a
-// group folds chunks g, g + G, ...  Results go to LDS (st_*[j] for position j).
+// group folds chunks g, g + G, ...  Results go to LDS (st_*[j] for position j;
+// st_zmax, when given, receives the greedy rows' largest raw target logit).
 template <int G, int WAVES>
 __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t slot0, int32_t s, int32_t nc,
                                      const PairChunk &q0, const ChunkArg *__restrict__ chunk_arg, ChunkArg arg0,
                                      float *st_mt, float *st_md, double *st_sp, double *st_sq, double *st_a,
-                                     double *st_h, int *st_bad, int *st_arg) {
+                                     double *st_h, int *st_bad, int *st_arg, float *st_zmax = nullptr) {
   constexpr int P = 64 / G;  // pairs per wavefront
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane % G;
   for (int32_t base = 0; base < s; base += WAVES * P) {
@@ -148,16 +169,7 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
           la = q.a;
           lh = q.h;
         } else {
-          const float nt = fmaxf(lmt, q.mt), nd = fmaxf(lmd, q.md);
-          const double d0t = double(lmt) - nt, d0d = double(lmd) - nd;
-          const double d1t = double(q.mt) - nt, d1d = double(q.md) - nd;
-          const double f0t = exp2_taylor(d0t), f0d = exp2_taylor(d0d), f1t = exp2_taylor(d1t), f1d = exp2_taylor(d1d);
-          la = f0t * (la + lsp * (d0t - d0d)) + f1t * (q.a + q.sp * (d1t - d1d));
-          lh = f0d * (lh + lsq * d0d) + f1d * (q.h + q.sq * d1d);
-          lsp = f0t * lsp + f1t * q.sp;
-          lsq = f0d * lsq + f1d * q.sq;
-          lmt = nt;
-          lmd = nd;
+          fold_pair_stats(lmt, lmd, lsp, lsq, la, lh, q.mt, q.md, q.sp, q.sq, q.a, q.h);
         }
       }
     }
@@ -176,8 +188,9 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
     ta = group_sum<G>(ta);
     th = group_sum<G>(th);
     int32_t arg = 0x7fffffff;
+    float zm = -INFINITY;
     if (chunk_arg) {  // the row argmax: smallest token among the chunks holding the row maximum
-      const float zm = group_max<G>(lz);
+      zm = group_max<G>(lz);
       arg = larg != 0x7fffffff && lz == zm ? larg : 0x7fffffff;
       arg = lanes::group_reduce<G>(arg, lanes::Min{});
     }
@@ -190,6 +203,7 @@ __device__ inline void combine_pairs(const PairChunk *__restrict__ part, int64_t
       st_h[j] = th;
       st_bad[j] = !(isfinite(mt) && isfinite(md) && isfinite(tsp) && isfinite(tsq) && isfinite(ta));
       st_arg[j] = arg;
+      if (st_zmax) st_zmax[j] = zm;
     }
   }
 }
@@ -486,5 +500,94 @@ __device__ inline void bonus_argmax_chunk(const char *trow, int64_t V, int64_t c
   }
 }
 
+
+// The inverse-CDF draw inside one row, by one wavefront, from the totals a
+// chunk pass left behind: weight(ch) is chunk ch's draw weight (fp64, in the
+// row's scale), subs holds 64 row partials of the 16 sub-block totals per
+// chunk (chunk-major), and target is the weight to pass, in [0, row total).
+// The rule at every level (chunk, sub-block, element) is the draw's: the last
+// position with positive weight whose exclusive prefix is <= the target.
+// Bonus rows (mode 2) carry a reference per chunk, chunk_ref(ch), and the row
+// scale row_ref.  Returns the row-local token id in every lane.
+template <int DT, bool VEC, typename WF, typename RF>
+__device__ inline int32_t draw_in_row(int32_t nc, WF weight, RF chunk_ref, float row_ref, double target,
+                                      const float *subs, const char *trow, const char *drow, int64_t V, int mode,
+                                      const DrawJob &job) {
+  const int lane = threadIdx.x & 63;
+  int32_t best = -1;
+  double best_excl = 0.0, base = 0.0;
+  for (int32_t c0 = 0; c0 < nc; c0 += 64) {
+    const int32_t ch = c0 + lane;
+    const double w = ch < nc ? weight(ch) : 0.0;
+    const lanes::Scan<double> sc = lanes::wave_scan(w);
+    const double incl = base + sc.incl;
+    const double excl = lane == 0 ? base : base + sc.excl;
+    const uint64_t cand = __ballot(ch < nc && w > 0.0 && excl <= target);
+    if (cand) {
+      const int l = 63 - __builtin_clzll(cand);
+      best = c0 + l;
+      best_excl = lanes::readlane(excl, l);
+    }
+    base = lanes::readlane(incl, 63);
+  }
+  const int32_t chunk = best >= 0 ? best : 0;
+  double rem = target - best_excl;
+  if (rem < 0.0) rem = 0.0;
+  const float ref = mode == 2 ? chunk_ref(chunk) : 0.f;
+  if (mode == 2) rem *= exp2_taylor(double(row_ref) - double(ref));  // into the chunk's own scale
+
+  // the sub-block
+  double sbw = 0.0;
+  if (lane < kSubs) {
+    const float *r = subs + int64_t(chunk) * 64;
+    sbw = double(((r[lane] + r[16 + lane]) + r[32 + lane]) + r[48 + lane]);
+  }
+  const lanes::Scan<double> ss = lanes::wave_scan(sbw);
+  const uint64_t scand = __ballot(lane < kSubs && sbw > 0.0 && ss.excl <= rem);
+  const int sb = scand ? 63 - __builtin_clzll(scand) : 0;
+  double rem2 = rem - lanes::readlane(ss.excl, sb);
+  if (rem2 < 0.0) rem2 = 0.0;
+
+  // its 512 logits, 8 consecutive per lane
+  const int64_t run0 = int64_t(chunk) * kChunk + int64_t(sb) * kSubLen + 8 * lane;
+  float w[8];
+  {
+    float zt[8];
+    load_run<DT, VEC, 8>(trow, V, run0, zt);
+    if (mode == 0) {
+      float zd[8];
+      load_run<DT, VEC, 8>(drow, V, run0, zd);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) w[i] = residual_weight(zt[i], zd[i], job);
+    } else if (mode == 1) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) w[i] = target_p_weight(zt[i], job);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) w[i] = bonus_weight(zt[i], job.scale, ref);
+    }
+  }
+  double run_total = 0.0;
+  int last = -1;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    run_total += double(w[i]);
+    if (w[i] > 0.0f) last = i;
+  }
+  const lanes::Scan<double> sr = lanes::wave_scan(run_total);
+  const uint64_t cand = __ballot(last >= 0 && sr.excl <= rem2);
+  const int winner = cand ? 63 - __builtin_clzll(cand) : 0;
+  int pick = last >= 0 ? last : 0;
+  double acc = sr.excl;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    acc += double(w[i]);
+    if (acc > rem2) {
+      pick = i;
+      break;
+    }
+  }
+  return lanes::readlane(int32_t(run0 + pick), winner);
+}
 }  // namespace
 }  // namespace dsde

@@ -158,3 +158,78 @@ def test_calibrate_sl_max_rejects_invalid_arguments(lib, over):
     a = dict(B=4, amax=FAKE, ksum=FAKE, kcnt=FAKE, kmax=FAKE, eps=1e-6, pooled=0, out=FAKE, stream=None)
     a.update(over)
     assert lib.dsde_calibrate_sl_max(*a.values()) == 1
+
+
+def test_shard_workspace_sizes(lib):
+    ws = lib.dsde_shard_workspace_bytes
+    assert ws(256, 1152, 16032, 8) > 0
+    assert ws(256, 1152, 16032, 8) > lib.dsde_verify_workspace_bytes(256, 1152, 16032, 8)
+    for bad in ((0, 0, 10, 4), (4, 0, 0, 4), (4, 0, 4194305, 4), (4, 17, 10, 4), (4, 0, 10, 64)):
+        assert ws(*bad) == 0, bad
+
+
+def shard_stats_args(**over):
+    a = dict(target=FAKE, draft=FAKE, dtype=1, V_shard=500, v_begin=500, V=1000, B=4, N=8, k_max=4, sl=FAKE,
+             cu_sl=FAKE, toks=FAKE, temp=FAKE, part=FAKE, err=FAKE, ws=FAKE, ws_bytes=1 << 30, stream=None)
+    a.update(over)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("over", [
+    dict(dtype=2), dict(V_shard=0), dict(v_begin=-1), dict(v_begin=501), dict(V=4194305), dict(V=0), dict(B=0),
+    dict(N=17), dict(k_max=64), dict(target=None), dict(draft=None), dict(sl=None), dict(cu_sl=None),
+    dict(toks=None), dict(temp=None), dict(part=None), dict(err=None), dict(ws=None),
+    dict(ws=ctypes.c_void_p(0x1001)),
+])
+def test_shard_stats_rejects_invalid_arguments(lib, over):
+    assert lib.dsde_shard_stats(*shard_stats_args(**over)) == 1
+
+
+def test_shard_stats_workspace_too_small(lib):
+    need = lib.dsde_shard_workspace_bytes(4, 8, 500, 4)
+    assert lib.dsde_shard_stats(*shard_stats_args(ws_bytes=need - 1)) == 2
+
+
+@pytest.mark.parametrize("over", [
+    dict(G=0), dict(G=1025), dict(V=0), dict(B=0), dict(N=17), dict(parts=None), dict(sl=None), dict(toks=None),
+    dict(u_acc=None), dict(u_res=None), dict(acc=None), dict(tokens=None), dict(kld=None), dict(jobs=None),
+    dict(err=None),
+])
+def test_shard_accept_rejects_invalid_arguments(lib, over):
+    a = dict(G=2, parts=FAKE, V=1000, B=4, N=8, k_max=4, sl=FAKE, cu_sl=FAKE, toks=FAKE, temp=FAKE, u_acc=FAKE,
+             u_res=FAKE, pad=-1, acc=FAKE, tokens=FAKE, kld=FAKE, lse=None, ent=None, jobs=FAKE, err=FAKE,
+             stream=None)
+    a.update(over)
+    assert lib.dsde_shard_accept(*a.values()) == 1
+
+
+@pytest.mark.parametrize("over", [
+    dict(dtype=2), dict(V_shard=0), dict(v_begin=-1), dict(B=0), dict(target=None), dict(draft=None),
+    dict(part=None), dict(jobs=None), dict(mass=None), dict(ws=None),
+])
+def test_shard_draw_mass_rejects_invalid_arguments(lib, over):
+    a = dict(target=FAKE, draft=FAKE, dtype=1, V_shard=500, v_begin=0, B=4, N=8, k_max=4, part=FAKE, jobs=FAKE,
+             mass=FAKE, ws=FAKE, ws_bytes=1 << 30, stream=None)
+    a.update(over)
+    assert lib.dsde_shard_draw_mass(*a.values()) == 1
+
+
+@pytest.mark.parametrize("over", [
+    dict(G=0), dict(g=-1), dict(g=2), dict(G=1025), dict(masses=None), dict(target=None), dict(draft=None),
+    dict(dtype=2), dict(jobs=None), dict(acc=None), dict(tokens=None), dict(drawn=None), dict(err=None),
+    dict(ws=None),
+])
+def test_shard_draw_pick_rejects_invalid_arguments(lib, over):
+    a = dict(G=2, g=1, masses=FAKE, target=FAKE, draft=FAKE, dtype=1, V_shard=500, v_begin=500, B=4, N=8,
+             k_max=4, jobs=FAKE, pad=-1, acc=FAKE, tokens=FAKE, drawn=FAKE, err=FAKE, ws=FAKE, ws_bytes=1 << 30,
+             stream=None)
+    a.update(over)
+    assert lib.dsde_shard_draw_pick(*a.values()) == 1
+
+
+def test_slice_bounds_tile_the_vocabulary():
+    import paper_2509_01083_amd as dsde
+    for V, G in ((128256, 8), (25281, 3), (17, 4), (100, 8), (1, 3), (152064, 7)):
+        b = dsde.slice_bounds(V, G)
+        assert b[0][0] == 0 and b[-1][1] == V and len(b) <= G
+        assert all(b[i][1] == b[i + 1][0] and b[i][0] < b[i][1] for i in range(len(b) - 1))
