@@ -59,6 +59,9 @@ def main():
 
     dsde.load()
     dev = torch.device("cuda:0")
+    if args.workload == "shard8":
+        print(json.dumps(run_shard(args, dev)), flush=True)
+        return
     cfg = W.CONFIGS[args.workload]
     if args.workload == "loop":
         print(json.dumps(run_loop(args, cfg, dev)), flush=True)
@@ -316,6 +319,107 @@ def run_loop(args, cfg, dev):
                             "min": float(np.min(caps)), "max": float(np.max(caps))},
                  "fraction_in_sl_min_branch": float(np.mean(min_branch)),
                  "note": "rows gathered from two pre-generated full-length pools; each step timed alone"},
+    }
+
+
+def run_shard(args, dev, G=8):
+    """One GPU's share of the b256 step with the vocabulary split eight ways:
+    shard 0's four calls on its 16,032-column slices (statistics, acceptance
+    from the gathered partials, draw mass, draw), then the signal update and
+    the SL rule, which run unchanged on every shard.  The other shards'
+    contributions to the two exchanges are computed before the timed region
+    (on this GPU, with the same calls); the exchanges themselves (RCCL
+    all-gathers) are not part of the measurement."""
+    import numpy as np
+    import torch
+
+    import paper_2509_01083_amd as dsde
+    import workloads as W
+    dsde.load()
+    cfg = W.CONFIGS["b256"]
+    sl = W.sample_sl(cfg, args.seed)
+    copies = [W.make_step(cfg, seed=args.seed + i, device=dev, sl=sl) for i in range(2)]
+    st = W.make_signal_state(cfg, seed=args.seed, device=dev)
+    s0 = copies[0]
+    B, N, V, k_max = s0.B, s0.N, s0.V, s0.k_max
+    esz = 2 if s0.target.dtype == torch.bfloat16 else 4
+    slices = dsde.slice_bounds(V, G)
+    v0, v1 = slices[0]
+    Vs = v1 - v0
+    ws = dsde.new_shard_workspace(B, N, Vs, k_max, device=dev)
+    prep = []
+    for s in copies:
+        full = dsde.verify_sharded(s.target, s.draft, s.sl, s.cu_sl, s.draft_tokens, s.temperature, s.u_acc,
+                                   s.u_res, k_max, slices)
+        prep.append(dict(step=s, t=s.target[:, v0:v1].contiguous(), d=s.draft[:, v0:v1].contiguous(),
+                         parts=full["parts"].clone(), masses=full["masses"].clone(),
+                         err=torch.empty(B, dtype=torch.int32, device=dev), out=None, sig=None, nxt=None,
+                         drawn=torch.empty(B, dtype=torch.int32, device=dev), ref_tokens=full["tokens"].clone(),
+                         ref_accepted=full["accepted"].clone()))
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+
+    def one(i, timed=False):
+        p = prep[i % 2]
+        s = p["step"]
+        if timed:
+            ev[0].record()
+        dsde.shard_stats(p["t"], p["d"], v0, V, s.sl, s.cu_sl, s.draft_tokens, s.temperature, k_max, ws,
+                         part=p["parts"][0], seq_err=p["err"])
+        if timed:
+            ev[1].record()
+        p["out"] = dsde.shard_accept(p["parts"], V, s.sl, s.cu_sl, s.draft_tokens, s.temperature, s.u_acc, s.u_res,
+                                     k_max, p["err"], out=p["out"])
+        if timed:
+            ev[2].record()
+        dsde.shard_draw_mass(p["t"], p["d"], v0, p["parts"][0], p["out"]["jobs"], k_max, ws, mass=p["masses"][0])
+        if timed:
+            ev[3].record()
+        dsde.shard_draw_pick(0, p["masses"], p["t"], p["d"], v0, p["out"]["jobs"], k_max, p["out"]["accepted"],
+                             p["out"]["tokens"], p["err"], ws, drawn=p["drawn"])
+        if timed:
+            ev[4].record()
+        p["sig"] = dsde.kld_signal(s.sl, s.cu_sl, p["out"]["kld"], st.hist, st.head, st.count, out=p["sig"])
+        p["nxt"] = dsde.next_sl(p["sig"]["sf"], p["sig"]["wvir"], st.sl_max, 2.0, k_max, out=p["nxt"])
+        if timed:
+            ev[5].record()
+
+    for i in range(args.warmup):
+        one(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        one(args.warmup + i)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    # per-call split from a second region with events between the calls
+    split = np.zeros(5)
+    for i in range(args.steps):
+        one(args.warmup + args.steps + i, timed=True)
+        torch.cuda.synchronize()
+        split += [ev[k].elapsed_time(ev[k + 1]) for k in range(5)]
+    split /= args.steps
+    # shard 0's decisions agree with the run of all shards: the accepted counts,
+    # and the whole token rows of the sequences whose token shard 0 drew
+    p = prep[(args.warmup + 2 * args.steps - 1) % 2]
+    own = p["drawn"] >= 0
+    agree = bool(torch.equal(p["out"]["accepted"], p["ref_accepted"]) and
+                 torch.equal(p["out"]["tokens"][own], p["ref_tokens"][own]))
+    rows = 2 * N + B
+    return {
+        "metric": METRIC, "value": rows / (ms * 1e-3), "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if esz == 2 else "fp32", "data": "synthetic",
+        "config": {"workload": "shard8", "B": B, "N": N, "V": V, "shard": 0, "shards": len(slices),
+                   "V_shard": Vs, "k_max": k_max, "seed": args.seed},
+        "note": "rows/s counts one shard's slices of the step's 2N+B rows; exchanges excluded",
+        "shard_bytes_per_step": rows * Vs * esz,
+        "shard_gbps_rows": rows * Vs * esz / (ms * 1e-3) / 1e9,
+        "ms_per_call": {"stats": split[0], "accept": split[1], "draw_mass": split[2], "draw_pick": split[3],
+                        "signal_and_sl": split[4]},
+        "draws_by_this_shard": int(own.sum()),
+        "decisions_match_all_shards_run": agree,
     }
 
 

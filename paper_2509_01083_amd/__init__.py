@@ -465,7 +465,8 @@ def verify_sharded(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u
     ascending, tiling [0, V)) run on one device, the exchanges being the gathered
     tensors themselves: the sharded path's results on one GPU, for tests and
     measurements.  Returns the dict of dsde_verify's outputs plus ``drawn``
-    (the all-reduce max of every shard's drawn[])."""
+    (the all-reduce max of every shard's drawn[]) and the two exchanged arrays,
+    ``parts`` [G, N, 64] and ``masses`` [G, B, 32]."""
     V = int(target.shape[1])
     B = int(sl.shape[0])
     N = int(draft.shape[0]) if draft is not None else 0
@@ -491,5 +492,7 @@ def verify_sharded(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u
              for g, (v0, t, d, ws) in enumerate(shards)]
     out["drawn"] = torch.stack(drawn).max(dim=0).values
     out["shard_seq_err"] = errs
+    out["parts"] = torch.stack(parts)
+    out["masses"] = masses
     return out
 
