@@ -233,10 +233,17 @@ def clone_state(st):
 WIDE = dict(W.CONFIGS["greedy"], B=1500, V=512)
 
 
-@pytest.mark.parametrize("name", ["tiny", "b64", "b256", "greedy", "wide"])
+@pytest.mark.parametrize("name", ["tiny", "b64", "b256", "greedy", "wide", "layout", "wide_layout"])
 def test_fused_step_equals_the_three_calls(gpu_lib, name):
-    cfg = WIDE if name == "wide" else W.CONFIGS[name]
+    """dsde_step against dsde_verify, dsde_kld_signal and dsde_next_sl in turn:
+    identical bits.  The layout cases break cu_sl, which flags every sequence
+    before any row is read; the SL rule still runs on the flagged batch."""
+    cfg = WIDE if name.startswith("wide") else W.CONFIGS["b64" if name == "layout" else name]
     step = W.make_step(cfg, seed=31, device="cuda")
+    if name.endswith("layout"):
+        cu = step.cu_sl.clone()
+        cu[1] += 1
+        step = W.Step(**{**step.__dict__, "cu_sl": cu})
     st = W.make_signal_state(cfg, seed=31, device="cuda")
     announce(f"fused step vs chain {name}")
     st_a, st_b = clone_state(st), clone_state(st)
@@ -252,11 +259,16 @@ def test_fused_step_equals_the_three_calls(gpu_lib, name):
     chain = {**v, **s_, **n_}
     for k in ("accepted", "tokens", "sl_next"):
         assert torch.equal(chain[k], f[k]), k
-    for k in ("kld", "draft_entropy", "mu_last", "var_short", "var_long", "wvir", "sf", "sl_hat", "sl_cap"):
+    written = ("mu_last", "var_short", "var_long", "wvir", "sf", "sl_hat", "sl_cap")
+    if not name.endswith("layout"):  # the KLD is not written under an invalid layout
+        written = ("kld", "draft_entropy") + written
+    for k in written:
         assert torch.equal(chain[k].view(torch.int32), f[k].view(torch.int32)), k
     assert torch.equal(st_a.hist.view(torch.int32), st_b.hist.view(torch.int32))
     assert torch.equal(st_a.head, st_b.head) and torch.equal(st_a.count, st_b.count)
     assert torch.equal(v["seq_err"] | s_["seq_err"] | n_["seq_err"], f["seq_err"])
+    if name.endswith("layout"):
+        assert (f["seq_err"].cpu().numpy() & 1).all()
 
 
 @pytest.mark.parametrize("name", ["b256", "lowacc", "b256g"])
