@@ -73,21 +73,29 @@ __global__ __launch_bounds__(1024) void setup_kernel(int32_t B, int64_t N, int32
 // ---------------------------------------------------------------------------
 
 // Greedy pairs: each wavefront's smallest token id holding the chunk maximum
-// M of the target row, into red[wave] (0xffffffff if none).  A thread's slots
-// ascend in token order in every layout, so its first slot equal to M is its
-// smallest such token.  `z(i)` is slot i of this thread's logits.
+// M of the target row, into red[wave] (0xffffffff if none).  Only a thread
+// whose own maximum `tmax` equals M holds it, so only those threads scan
+// their slots and only wavefronts holding one reduce (in most chunks one
+// wavefront of four).  A thread's slots ascend in token order in every
+// layout, so its first slot equal to M is its smallest such token.  `z(i)` is
+// slot i of this thread's logits.
 template <int DT, bool VEC, typename Z>
-__device__ __forceinline__ void wave_chunk_argmax(float M, Z z, int64_t chunk, uint32_t *red) {
+__device__ __forceinline__ void wave_chunk_argmax(float M, float tmax, Z z, int64_t chunk, uint32_t *red) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  int first = -1;
+  uint32_t best = 0xffffffffu;
+  if (tmax == M) {
+    int first = -1;
 #pragma unroll
-  for (int i = kEltsPerThread - 1; i >= 0; --i)
-    if (z(i) == M) first = i;
-  uint32_t best = first >= 0 ? uint32_t(Layout<DT, VEC>::index(chunk, first, t)) : 0xffffffffu;
+    for (int i = kEltsPerThread - 1; i >= 0; --i)
+      if (z(i) == M) first = i;
+    if (first >= 0) best = uint32_t(Layout<DT, VEC>::index(chunk, first, t));
+  }
+  if (__ballot(best != 0xffffffffu)) {
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint32_t y = __shfl_xor(best, o);
-    best = y < best ? y : best;
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint32_t y = __shfl_xor(best, o);
+      best = y < best ? y : best;
+    }
   }
   if (lane == 0) red[wave] = best;
 }
@@ -157,9 +165,11 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
   const RawBf16 rd_ = load_raw_bf16(drow, V, chunk, t);
 
   // chunk maxima -> the reference shifts every exponential of the chunk uses
-  const float Mt = block_max(raw_max(rt_), red[0]);
+  const float tmt = raw_max(rt_);
+  const float Mt = block_max(tmt, red[0]);
   const float Md = block_max(raw_max(rd_), red[1]);
-  if (greedy) wave_chunk_argmax<DSDE_BF16, true>(Mt, [&](int i) { return pick_bf16(rt_, i); }, chunk, red_arg);
+  if (greedy)
+    wave_chunk_argmax<DSDE_BF16, true>(Mt, tmt, [&](int i) { return pick_bf16(rt_, i); }, chunk, red_arg);
   const float rt = Mt * c, rd = Md * c;
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   acc_vec(rt_.v0, rd_.v0, c, rt, rd, s);
@@ -224,7 +234,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
   }
   const float Mt = block_max(mt, red[0]);
   const float Md = block_max(md, red[1]);
-  if (greedy) wave_chunk_argmax<DT, VEC>(Mt, [&](int i) { return zt[i]; }, chunk, red_arg);
+  if (greedy) wave_chunk_argmax<DT, VEC>(Mt, mt, [&](int i) { return zt[i]; }, chunk, red_arg);
   const float rt = Mt * c, rd = Md * c;
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
