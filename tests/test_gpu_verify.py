@@ -336,3 +336,37 @@ def test_greedy_ignores_uniforms_and_flags_a_bad_bonus_row(gpu_lib):
     assert list(got["seq_err"]) == [0, 0, 4]
     assert list(got["accepted"][:2]) == [2, 2]
     assert np.isfinite(got["kld"]).all()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_longest_speculation(gpu_lib, dtype):
+    """k_max = DSDE_MAX_K = 63: a sequence drafting 63 tokens that all pass
+    (identical rows, bonus draw from row 63), one with a long accepted run
+    ending in a rejection, a greedy one rejecting at position 40, and SL = 0
+    and a short sequence beside them; unsharded and over three slices."""
+    rng = np.random.default_rng(63)
+    V, k_max = 9000, 63
+    sls = [63, 0, 17, 63, 63]
+    target, draft, tokens, u_acc, u_res = random_arrays(rng, sls, V)
+    sl, cu = packed_layout(sls)
+    draft[cu[0]:cu[1]] = target[0:63]                                  # seq 0: p = q
+    u_acc[cu[0]:cu[1]] = 0.999
+    draft[cu[3]:cu[4]] = target[cu[3] + 3:cu[4] + 3] + rng.normal(0, 0.02, (63, V))  # seq 3: q close to p
+    u_acc[cu[3]:cu[4]] = 0.05
+    u_acc[cu[3] + 50] = 0.99999                                          # a likely rejection late in the run
+    temps = [1.0, 0.7, 0.9, 1.0, 0.0]
+    step = step_from_arrays(target, draft, sls, tokens, temps, u_acc, u_res, k_max, dtype)
+    # seq 4 (greedy): draft the target argmax of rows 0..39, then a token that is not
+    rows = step.target[cu[4] + 4:cu[4] + 4 + 63].float().cpu().numpy()
+    greedy_tok = rows.argmax(axis=1).astype(np.int32)
+    greedy_tok[40] = (greedy_tok[40] + 1) % V
+    toks = step.draft_tokens.clone()
+    toks[cu[4]:cu[5]] = torch.as_tensor(greedy_tok, device="cuda")
+    step = W.Step(**{**step.__dict__, "draft_tokens": toks})
+    got, _, rep = check_step(gpu_lib, step, f"k_max 63 {dtype}")
+    assert got["accepted"][0] == 63 and got["accepted"][4] == 40, got["accepted"]
+    assert got["accepted"][3] > 10, got["accepted"]
+    assert rep["errored"] == 0
+    import paper_2509_01083_amd as dsde
+    from tests.test_gpu_shard import check_sharded
+    check_sharded(dsde, step, dsde.slice_bounds(V, 3), f"k_max 63 {dtype} sharded")
