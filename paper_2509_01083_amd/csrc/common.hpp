@@ -123,6 +123,9 @@ struct VerifyArgs {
   hipStream_t stream;
   hipEvent_t prof_start, prof_stop;
   const SignalArgs *signal;  // non-null: fused signal update and SL rule
+  // subtracted from each drafted token before its logits are gathered: the
+  // first id of a vocabulary slice whose logits the rows hold, else 0
+  int64_t token_base = 0;
 };
 
 int launch_verify(const VerifyArgs &a);

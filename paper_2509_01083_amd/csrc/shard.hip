@@ -3,10 +3,11 @@
 // calls and the exchanges between them are described with dsde_shard_stats in
 // dsde.h).  Each call is the matching part of dsde_verify restricted to the
 // shard's slice:
-//   call 1  shard_tokens_kernel (drafted tokens as slice indices), then the
-//           set-up and statistics kernels of dsde_verify on the slice
-//           (stats.hip), then shard_combine_kernel: the chunk partials of
-//           each drafted pair folded into one slice partial.
+//   call 1  the set-up and statistics kernels of dsde_verify on the slice
+//           (stats.hip; drafted tokens are offset by the slice's first id,
+//           so tokens outside it gather nothing), then shard_combine_kernel:
+//           the chunk partials of each drafted pair folded into one slice
+//           partial.
 //   call 2  shard_accept_kernel: one wavefront per sequence folds the G slice
 //           partials in shard order (fp64), then KLD, acceptance and the draw
 //           job exactly as the per-sequence kernel of dsde_verify.
@@ -43,25 +44,14 @@ constexpr int kShardWaves = kShardThreads / 64;
 
 // ---- call 1 --------------------------------------------------------------
 
-// The drafted tokens as indices into the slice, -1 for tokens it does not
-// hold (the statistics kernel then gathers nothing for them).
-__global__ __launch_bounds__(256) void shard_tokens_kernel(int64_t N, const int32_t *__restrict__ tokens,
-                                                           int64_t v_begin, int64_t V_shard,
-                                                           int32_t *__restrict__ local) {
-  const int64_t k = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (k >= N) return;
-  const int64_t l = int64_t(tokens[k]) - v_begin;
-  local[k] = l >= 0 && l < V_shard ? int32_t(l) : -1;
-}
-
 // One workgroup per sequence: the chunk partials of each drafted pair folded
 // into the slice partial (the combine of the per-sequence kernel).
 template <int GL>
 __global__ __launch_bounds__(kShardThreads) void shard_combine_kernel(
     const PairChunk *__restrict__ part, const ChunkArg *__restrict__ chunk_arg, const Gathered *__restrict__ gath,
-    const int32_t *__restrict__ sl, const int32_t *__restrict__ cu_sl, const int32_t *__restrict__ local_tokens,
+    const int32_t *__restrict__ sl, const int32_t *__restrict__ cu_sl, const int32_t *__restrict__ draft_tokens,
     const float *__restrict__ temperature, const uint32_t *__restrict__ seq_err, int32_t k_max, int32_t nc,
-    int64_t v_begin, dsde_shard_partial *__restrict__ out) {
+    int64_t v_begin, int64_t V_shard, dsde_shard_partial *__restrict__ out) {
   __shared__ float st_mt[DSDE_MAX_K + 1], st_md[DSDE_MAX_K + 1], st_zmax[DSDE_MAX_K + 1];
   __shared__ double st_sp[DSDE_MAX_K + 1], st_sq[DSDE_MAX_K + 1], st_a[DSDE_MAX_K + 1], st_h[DSDE_MAX_K + 1];
   __shared__ int st_bad[DSDE_MAX_K + 1], st_arg[DSDE_MAX_K + 1];
@@ -90,7 +80,8 @@ __global__ __launch_bounds__(kShardThreads) void shard_combine_kernel(
     r.sq = st_sq[t];
     r.a = st_a[t];
     r.h = st_h[t];
-    r.has_token = local_tokens[first + t] >= 0;
+    const int64_t l = int64_t(draft_tokens[first + t]) - v_begin;  // the token's index in the slice
+    r.has_token = l >= 0 && l < V_shard;
     const Gathered gz = r.has_token ? gath[slot0 + t] : Gathered{0.f, 0.f};
     r.zt = gz.zt;
     r.zd = gz.zd;
@@ -545,11 +536,7 @@ int launch_shard_stats(const ShardRows &r, int64_t V, const int32_t *sl, const i
   (void)V;
   const ShardLayout L = shard_layout(r.B, r.N, r.V_shard, r.k_max);
   char *ws = (char *)r.workspace;
-  int32_t *local = (int32_t *)(ws + L.local_tokens);
   (void)hipGetLastError();
-  if (r.N > 0)
-    shard_tokens_kernel<<<dim3(unsigned((r.N + 255) / 256)), dim3(256), 0, r.stream>>>(r.N, draft_tokens, r.v_begin,
-                                                                                      r.V_shard, local);
   VerifyArgs a{};
   a.target = r.target;
   a.draft = r.draft;
@@ -560,7 +547,8 @@ int launch_shard_stats(const ShardRows &r, int64_t V, const int32_t *sl, const i
   a.k_max = r.k_max;
   a.sl = sl;
   a.cu_sl = cu_sl;
-  a.draft_tokens = local;
+  a.draft_tokens = draft_tokens;
+  a.token_base = r.v_begin;
   a.temperature = temperature;
   a.seq_err = seq_err;
   a.workspace = r.workspace;
@@ -574,14 +562,14 @@ int launch_shard_stats(const ShardRows &r, int64_t V, const int32_t *sl, const i
     const int32_t nc = int32_t(num_chunks(r.V_shard));
     const dim3 grid(unsigned(r.B)), block(kShardThreads);
     if (nc <= 16)
-      shard_combine_kernel<16><<<grid, block, 0, r.stream>>>(pc, cargs, gath, sl, cu_sl, local, temperature, seq_err,
-                                                             r.k_max, nc, r.v_begin, part);
+      shard_combine_kernel<16><<<grid, block, 0, r.stream>>>(pc, cargs, gath, sl, cu_sl, draft_tokens, temperature,
+                                                             seq_err, r.k_max, nc, r.v_begin, r.V_shard, part);
     else if (nc <= 32)
-      shard_combine_kernel<32><<<grid, block, 0, r.stream>>>(pc, cargs, gath, sl, cu_sl, local, temperature, seq_err,
-                                                             r.k_max, nc, r.v_begin, part);
+      shard_combine_kernel<32><<<grid, block, 0, r.stream>>>(pc, cargs, gath, sl, cu_sl, draft_tokens, temperature,
+                                                             seq_err, r.k_max, nc, r.v_begin, r.V_shard, part);
     else
-      shard_combine_kernel<64><<<grid, block, 0, r.stream>>>(pc, cargs, gath, sl, cu_sl, local, temperature, seq_err,
-                                                             r.k_max, nc, r.v_begin, part);
+      shard_combine_kernel<64><<<grid, block, 0, r.stream>>>(pc, cargs, gath, sl, cu_sl, draft_tokens, temperature,
+                                                             seq_err, r.k_max, nc, r.v_begin, r.V_shard, part);
   }
   return hipGetLastError() == hipSuccess ? DSDE_OK : DSDE_DEVICE_ERROR;
 }

@@ -7,11 +7,11 @@
 namespace dsde {
 
 // One shard's workspace: the statistics pass's buffers for the slice width,
-// then the drafted tokens as slice indices, and the draw's chunk totals of
-// every sequence (call 3 writes them, call 4 reads them).
+// then the draw's chunk totals of every sequence (call 3 writes them, call 4
+// reads them).
 struct ShardLayout {
   WorkspaceLayout stats;
-  size_t local_tokens, ch_w, ch_ref, ch_bad, sub, total;
+  size_t ch_w, ch_ref, ch_bad, sub, total;
 };
 
 inline ShardLayout shard_layout(int32_t B, int64_t N, int64_t V_shard, int32_t k_max) {
@@ -19,8 +19,6 @@ inline ShardLayout shard_layout(int32_t B, int64_t N, int64_t V_shard, int32_t k
   L.stats = workspace_layout(B, N, V_shard, k_max);
   const size_t cells = size_t(B) * size_t(num_chunks(V_shard));
   size_t off = L.stats.total;
-  L.local_tokens = off;
-  off += align_up(sizeof(int32_t) * size_t(N > 0 ? N : 1));
   L.ch_w = off;
   off += align_up(sizeof(double) * cells);
   L.ch_ref = off;

@@ -146,7 +146,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
                                                              const void *__restrict__ draft, int64_t V, int32_t nc,
                                                              const WorkItem *__restrict__ work,
                                                              const int32_t *__restrict__ draft_tokens,
-                                                             PairChunk *__restrict__ out,
+                                                             int64_t token_base, PairChunk *__restrict__ out,
                                                              Gathered *__restrict__ gathered,
                                                              ChunkArg *__restrict__ chunk_arg) {
   __shared__ float red[6][kWaves];
@@ -179,7 +179,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
 
   // the logits at the drafted token, from registers
   // a token outside [0, V) never matches (its sequence is flagged later)
-  const int64_t local = int64_t(draft_tokens[w.pair]) - chunk * kChunk;
+  const int64_t local = int64_t(draft_tokens[w.pair]) - token_base - chunk * kChunk;
   if (local >= 0 && local < kChunk) {
     int ot, oi;
     Layout<DSDE_BF16, true>::owner(local, &ot, &oi);
@@ -207,7 +207,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
                                                                 const void *__restrict__ draft, int64_t V,
                                                                 int32_t nc, const WorkItem *__restrict__ work,
                                                                 const int32_t *__restrict__ draft_tokens,
-                                                                PairChunk *__restrict__ out,
+                                                                int64_t token_base, PairChunk *__restrict__ out,
                                                                 Gathered *__restrict__ gathered,
                                                                 ChunkArg *__restrict__ chunk_arg) {
   __shared__ float red[6][kWaves];
@@ -243,7 +243,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
     acc_pair(zt[i + 1], zd[i + 1], c, rt, rd, s[4], s[5], s[6], s[7]);
   }
   // a token outside [0, V) never matches (its sequence is flagged later)
-  const int64_t local = int64_t(draft_tokens[w.pair]) - chunk * kChunk;
+  const int64_t local = int64_t(draft_tokens[w.pair]) - token_base - chunk * kChunk;
   if (local >= 0 && local < kChunk) {
     int ot, oi;
     Layout<DT, VEC>::owner(local, &ot, &oi);
@@ -297,18 +297,20 @@ void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gat
   const void *T = a.target, *D = a.draft;
   const int64_t V = a.V;
   const int32_t *tokens = a.draft_tokens;
+  const int64_t base = a.token_base;
   const WorkItem *w = work;
   if (a.dtype == DSDE_BF16 && vec)
-    launch_timed(stats_kernel_bf16, grid, block, a.stream, done, T, D, V, nc, w, tokens, part, gath, chunk_arg);
+    launch_timed(stats_kernel_bf16, grid, block, a.stream, done, T, D, V, nc, w, tokens, base, part, gath,
+                 chunk_arg);
   else if (a.dtype == DSDE_BF16)
-    launch_timed(stats_kernel_generic<DSDE_BF16, false>, grid, block, a.stream, done, T, D, V, nc, w, tokens, part,
-                 gath, chunk_arg);
+    launch_timed(stats_kernel_generic<DSDE_BF16, false>, grid, block, a.stream, done, T, D, V, nc, w, tokens, base,
+                 part, gath, chunk_arg);
   else if (vec)
-    launch_timed(stats_kernel_generic<DSDE_FP32, true>, grid, block, a.stream, done, T, D, V, nc, w, tokens, part,
-                 gath, chunk_arg);
+    launch_timed(stats_kernel_generic<DSDE_FP32, true>, grid, block, a.stream, done, T, D, V, nc, w, tokens, base,
+                 part, gath, chunk_arg);
   else
-    launch_timed(stats_kernel_generic<DSDE_FP32, false>, grid, block, a.stream, done, T, D, V, nc, w, tokens, part,
-                 gath, chunk_arg);
+    launch_timed(stats_kernel_generic<DSDE_FP32, false>, grid, block, a.stream, done, T, D, V, nc, w, tokens, base,
+                 part, gath, chunk_arg);
 }
 
 }  // namespace dsde
