@@ -339,8 +339,8 @@ def run_loop(args, cfg, dev):
 def run_shard(args, dev, G=8):
     """One GPU's share of the b256 step with the vocabulary split eight ways:
     shard 0's four calls on its 16,032-column slices (statistics, acceptance
-    from the gathered partials, draw mass, draw), then the signal update and
-    the SL rule, which run unchanged on every shard.  The other shards'
+    from the gathered partials with the signal update and the SL rule fused
+    behind it, draw mass, draw).  The other shards'
     contributions to the two exchanges are computed before the timed region
     (on this GPU, with the same calls); the exchanges themselves (RCCL
     all-gathers) are not part of the measurement."""
@@ -367,10 +367,10 @@ def run_shard(args, dev, G=8):
                                    s.u_res, k_max, slices)
         prep.append(dict(step=s, t=s.target[:, v0:v1].contiguous(), d=s.draft[:, v0:v1].contiguous(),
                          parts=full["parts"].clone(), masses=full["masses"].clone(),
-                         err=torch.empty(B, dtype=torch.int32, device=dev), out=None, sig=None, nxt=None,
+                         err=torch.empty(B, dtype=torch.int32, device=dev), out=None,
                          drawn=torch.empty(B, dtype=torch.int32, device=dev), ref_tokens=full["tokens"].clone(),
                          ref_accepted=full["accepted"].clone()))
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
 
     def one(i, timed=False):
         p = prep[i % 2]
@@ -381,8 +381,9 @@ def run_shard(args, dev, G=8):
                          part=p["parts"][0], seq_err=p["err"])
         if timed:
             ev[1].record()
-        p["out"] = dsde.shard_accept(p["parts"], V, s.sl, s.cu_sl, s.draft_tokens, s.temperature, s.u_acc, s.u_res,
-                                     k_max, p["err"], out=p["out"])
+        p["out"] = dsde.shard_accept_step(p["parts"], V, s.sl, s.cu_sl, s.draft_tokens, s.temperature, s.u_acc,
+                                          s.u_res, k_max, p["err"], st.hist, st.head, st.count, st.sl_max,
+                                          out=p["out"])
         if timed:
             ev[2].record()
         dsde.shard_draw_mass(p["t"], p["d"], v0, p["parts"][0], p["out"]["jobs"], k_max, ws, mass=p["masses"][0])
@@ -392,10 +393,6 @@ def run_shard(args, dev, G=8):
                              p["out"]["tokens"], p["err"], ws, drawn=p["drawn"])
         if timed:
             ev[4].record()
-        p["sig"] = dsde.kld_signal(s.sl, s.cu_sl, p["out"]["kld"], st.hist, st.head, st.count, out=p["sig"])
-        p["nxt"] = dsde.next_sl(p["sig"]["sf"], p["sig"]["wvir"], st.sl_max, 2.0, k_max, out=p["nxt"])
-        if timed:
-            ev[5].record()
 
     for i in range(args.warmup):
         one(i)
@@ -408,11 +405,11 @@ def run_shard(args, dev, G=8):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
     # per-call split from a second region with events between the calls
-    split = np.zeros(5)
+    split = np.zeros(4)
     for i in range(args.steps):
         one(args.warmup + args.steps + i, timed=True)
         torch.cuda.synchronize()
-        split += [ev[k].elapsed_time(ev[k + 1]) for k in range(5)]
+        split += [ev[k].elapsed_time(ev[k + 1]) for k in range(4)]
     split /= args.steps
     # shard 0's decisions agree with the run of all shards: the accepted counts,
     # and the whole token rows of the sequences whose token shard 0 drew
@@ -430,8 +427,8 @@ def run_shard(args, dev, G=8):
         "note": "rows/s counts one shard's slices of the step's 2N+B rows; exchanges excluded",
         "shard_bytes_per_step": rows * Vs * esz,
         "shard_gbps_rows": rows * Vs * esz / (ms * 1e-3) / 1e9,
-        "ms_per_call": {"stats": split[0], "accept": split[1], "draw_mass": split[2], "draw_pick": split[3],
-                        "signal_and_sl": split[4]},
+        "ms_per_call": {"stats": split[0], "accept_signal_sl": split[1], "draw_mass": split[2],
+                        "draw_pick": split[3]},
         "draws_by_this_shard": int(own.sum()),
         "decisions_match_all_shards_run": agree,
     }

@@ -348,6 +348,27 @@ int32_t dsde_shard_accept(int32_t G, const dsde_shard_partial *parts, int64_t V,
                           dsde_draw_job *jobs, uint32_t *seq_err, void *stream);
 
 /*
+ * Call 2 fused with the signal update and the SL rule (Sec. 3.1.2, Eqs. 2-11):
+ * dsde_shard_accept, then dsde_kld_signal on the KLD it produces, then
+ * dsde_next_sl, with the arguments of those calls (see them for meaning,
+ * layout and ownership) in two launches instead of three; the outputs are
+ * bit-identical to the three calls in sequence and seq_err is the OR of their
+ * error bits, except that a layout error also skips the signal update (as in
+ * dsde_step).  Every GPU of the split holds the same KLD after the exchange,
+ * so each may run this on its own copy of the controller state.
+ * For serving loops that run the complete sharded step.
+ */
+int32_t dsde_shard_accept_step(int32_t G, const dsde_shard_partial *parts, int64_t V, int32_t B, int64_t N,
+                               int32_t k_max, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
+                               const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
+                               int32_t *accepted, int32_t *tokens, float *kld, double *row_lse,
+                               float *draft_entropy, dsde_draw_job *jobs, float *hist, int32_t *head, int32_t *count,
+                               int32_t W, int32_t n_short, int32_t n_long, float delta, float eps, float *mu_last,
+                               float *var_short, float *var_long, float *wvir, float *sf, const float *sl_max,
+                               float sl_min, int32_t sl_hi, const int32_t *budget, float *sl_hat, float *sl_cap,
+                               int32_t *sl_next, uint32_t *seq_err, void *stream);
+
+/*
  * Call 3: this slice's share of each sequence's draw weight (it reads the
  * slice of the first rejected pair, or of the bonus row, once) into mass [B];
  * the slice's chunk totals stay in the workspace for call 4.

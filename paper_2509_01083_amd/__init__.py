@@ -21,7 +21,7 @@ MAX_K = 63
 EXPORTS = ("dsde_abi_version", "dsde_status_string", "dsde_verify_workspace_bytes", "dsde_verify",
            "dsde_step", "dsde_kld_signal", "dsde_next_sl", "dsde_calibration_update", "dsde_calibrate_sl_max",
            "dsde_set_profile_events", "dsde_stream_read", "dsde_shard_workspace_bytes", "dsde_shard_stats",
-           "dsde_shard_accept", "dsde_shard_draw_mass", "dsde_shard_draw_pick")
+           "dsde_shard_accept", "dsde_shard_accept_step", "dsde_shard_draw_mass", "dsde_shard_draw_pick")
 # sizes of the records the vocabulary-shard calls exchange (dsde_shard_partial,
 # dsde_draw_job, dsde_shard_mass); kept as raw bytes on the Python side
 SHARD_PARTIAL_BYTES, DRAW_JOB_BYTES, SHARD_MASS_BYTES = 64, 44, 32
@@ -73,6 +73,10 @@ def load(path: str = LIB_PATH):
     lib.dsde_shard_stats.argtypes = [P, P, i32, i64, i64, i64, i32, i64, i32, P, P, P, P, P, P, P, sz, P]
     lib.dsde_shard_accept.restype = i32
     lib.dsde_shard_accept.argtypes = [i32, P, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P, P, P, P, P]
+    lib.dsde_shard_accept_step.restype = i32
+    lib.dsde_shard_accept_step.argtypes = [i32, P, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P, P, P,
+                                           P, P, P, i32, i32, i32, f32, f32, P, P, P, P, P,
+                                           P, f32, i32, P, P, P, P, P, P]
     lib.dsde_shard_draw_mass.restype = i32
     lib.dsde_shard_draw_mass.argtypes = [P, P, i32, i64, i64, i32, i64, i32, P, P, P, P, sz, P]
     lib.dsde_shard_draw_pick.restype = i32
@@ -371,12 +375,9 @@ def shard_stats(target, draft, v_begin, V, sl, cu_sl, draft_tokens, temperature,
     return part, seq_err
 
 
-def shard_accept(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, seq_err, pad_id=-1,
-                 row_lse=None, draft_entropy=False, out=None, stream=None):
-    """``dsde_shard_accept`` (call 2) from the gathered partials parts [G, N, 64]
-    (uint8, shard order).  seq_err (call 1's) is updated in place.  Returns a dict
-    with accepted, tokens, kld, seq_err, jobs [B, 44] uint8 (and draft_entropy)."""
-    lib = load()
+def _shard_accept_call(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, seq_err, pad_id,
+                       row_lse, draft_entropy, out):
+    """Output buffers and the leading ctypes arguments shared by the two call-2 entry points."""
     G = int(parts.shape[0])
     B = int(sl.shape[0])
     N = int(draft_tokens.shape[0]) if draft_tokens is not None else 0
@@ -394,19 +395,63 @@ def shard_accept(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k
     ent = out.get("draft_entropy") if draft_entropy else None
     if N > 0 and int(parts.shape[1]) != N:
         parts = parts[:, :N].contiguous()
-    rc = lib.dsde_shard_accept(
-        G, _ptr(parts, torch.uint8, G * N * SHARD_PARTIAL_BYTES, "parts") if N > 0 else None, int(V), B, N, k_max,
-        _ptr(sl, torch.int32, B, "sl"), _ptr(cu_sl, torch.int32, B + 1, "cu_sl"),
-        _ptr(draft_tokens, torch.int32, N, "draft_tokens") if N > 0 else None,
-        _ptr(temperature, torch.float32, B, "temperature"),
-        _ptr(u_acc, torch.float32, N, "u_acc") if N > 0 else None, _ptr(u_res, torch.float32, B, "u_res"),
-        int(pad_id), _ptr(out["accepted"], torch.int32, B, "accepted"),
-        _ptr(out["tokens"], torch.int32, B * (k_max + 1), "tokens"),
-        _ptr(out["kld"], torch.float32, N, "kld") if N > 0 else None,
-        _ptr(row_lse, torch.float64, 2 * N, "row_lse") if row_lse is not None else None,
-        _ptr(ent, torch.float32, N, "draft_entropy") if ent is not None and N > 0 else None,
-        _ptr(out["jobs"], torch.uint8, B * DRAW_JOB_BYTES, "jobs"), _ptr(seq_err, None, B, "seq_err"),
-        _stream(stream))
+    args = [G, _ptr(parts, torch.uint8, G * N * SHARD_PARTIAL_BYTES, "parts") if N > 0 else None, int(V), B, N,
+            k_max, _ptr(sl, torch.int32, B, "sl"), _ptr(cu_sl, torch.int32, B + 1, "cu_sl"),
+            _ptr(draft_tokens, torch.int32, N, "draft_tokens") if N > 0 else None,
+            _ptr(temperature, torch.float32, B, "temperature"),
+            _ptr(u_acc, torch.float32, N, "u_acc") if N > 0 else None, _ptr(u_res, torch.float32, B, "u_res"),
+            int(pad_id), _ptr(out["accepted"], torch.int32, B, "accepted"),
+            _ptr(out["tokens"], torch.int32, B * (k_max + 1), "tokens"),
+            _ptr(out["kld"], torch.float32, N, "kld") if N > 0 else None,
+            _ptr(row_lse, torch.float64, 2 * N, "row_lse") if row_lse is not None else None,
+            _ptr(ent, torch.float32, N, "draft_entropy") if ent is not None and N > 0 else None,
+            _ptr(out["jobs"], torch.uint8, B * DRAW_JOB_BYTES, "jobs")]
+    return out, args, parts
+
+
+def shard_accept(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, seq_err, pad_id=-1,
+                 row_lse=None, draft_entropy=False, out=None, stream=None):
+    """``dsde_shard_accept`` (call 2) from the gathered partials parts [G, N, 64]
+    (uint8, shard order).  seq_err (call 1's) is updated in place.  Returns a dict
+    with accepted, tokens, kld, seq_err, jobs [B, 44] uint8 (and draft_entropy)."""
+    lib = load()
+    out, args, _keep = _shard_accept_call(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max,
+                                          seq_err, pad_id, row_lse, draft_entropy, out)
+    B = int(sl.shape[0])
+    _check(lib.dsde_shard_accept(*args, _ptr(seq_err, None, B, "seq_err"), _stream(stream)))
+    return out
+
+
+def shard_accept_step(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, seq_err, hist, head,
+                      count, sl_max, n_short=10, n_long=30, delta=0.85, eps=1e-6, sl_min=2.0, sl_hi=None, pad_id=-1,
+                      row_lse=None, draft_entropy=False, budget=None, out=None, stream=None):
+    """``dsde_shard_accept_step``: call 2 with the signal update and the SL rule
+    fused behind it (hist/head/count updated in place).  Returns the outputs of
+    shard_accept plus mu_last, var_short, var_long, wvir, sf, sl_hat, sl_cap,
+    sl_next."""
+    lib = load()
+    out, args, _keep = _shard_accept_call(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max,
+                                          seq_err, pad_id, row_lse, draft_entropy, out)
+    B = int(sl.shape[0])
+    W = int(hist.shape[1])
+    sl_hi = k_max if sl_hi is None else sl_hi
+    dev = sl.device
+    f32 = torch.float32
+    for k in ("mu_last", "var_short", "var_long", "wvir", "sf", "sl_hat"):
+        if k not in out:
+            out[k] = torch.empty(B, dtype=f32, device=dev)
+    if "sl_cap" not in out:
+        out["sl_cap"] = torch.empty(1, dtype=f32, device=dev)
+    if "sl_next" not in out:
+        out["sl_next"] = torch.empty(B, dtype=torch.int32, device=dev)
+    rc = lib.dsde_shard_accept_step(
+        *args, _ptr(hist, f32, B * W, "hist"), _ptr(head, torch.int32, B, "head"),
+        _ptr(count, torch.int32, B, "count"), W, n_short, n_long, float(delta), float(eps),
+        _ptr(out["mu_last"], f32, B), _ptr(out["var_short"], f32, B), _ptr(out["var_long"], f32, B),
+        _ptr(out["wvir"], f32, B), _ptr(out["sf"], f32, B), _ptr(sl_max, f32, B, "sl_max"), float(sl_min),
+        int(sl_hi), _ptr(budget, torch.int32, B, "budget") if budget is not None else None,
+        _ptr(out["sl_hat"], f32, B), _ptr(out["sl_cap"], f32, 1), _ptr(out["sl_next"], torch.int32, B),
+        _ptr(seq_err, None, B, "seq_err"), _stream(stream))
     _check(rc)
     return out
 

@@ -89,6 +89,39 @@ int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t
   return dsde::launch_verify(a);
 }
 
+// The signal and SL-rule arguments of the fused calls, checked and packed.
+static int32_t signal_args(float *hist, int32_t *head, int32_t *count, int32_t W, int32_t n_short, int32_t n_long,
+                           float delta, float eps, float *mu_last, float *var_short, float *var_long, float *wvir,
+                           float *sf, const float *sl_max, float sl_min, int32_t sl_hi, const int32_t *budget,
+                           float *sl_hat, float *sl_cap, int32_t *sl_next, dsde::SignalArgs *sg) {
+  if (W < 1 || n_short < 1 || n_short > n_long) return DSDE_INVALID_ARG;
+  if (!(delta > 0.0f && delta <= 1.0f) || !(eps >= 0.0f) || !isfinite(eps)) return DSDE_INVALID_ARG;
+  if (!hist || !head || !count || !mu_last || !var_short || !var_long || !wvir || !sf) return DSDE_INVALID_ARG;
+  if (!isfinite(sl_min) || ceilf(sl_min) > float(sl_hi)) return DSDE_INVALID_ARG;
+  if (!sl_max || !sl_hat || !sl_cap || !sl_next) return DSDE_INVALID_ARG;
+  sg->hist = hist;
+  sg->head = head;
+  sg->count = count;
+  sg->W = W;
+  sg->n_short = n_short;
+  sg->n_long = n_long;
+  sg->delta = delta;
+  sg->eps = eps;
+  sg->mu_last = mu_last;
+  sg->var_short = var_short;
+  sg->var_long = var_long;
+  sg->wvir = wvir;
+  sg->sf = sf;
+  sg->sl_max = sl_max;
+  sg->sl_min = sl_min;
+  sg->sl_hi = sl_hi;
+  sg->budget = budget;
+  sg->sl_hat = sl_hat;
+  sg->sl_cap = sl_cap;
+  sg->sl_next = sl_next;
+  return DSDE_OK;
+}
+
 int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
                   int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
                   const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
@@ -104,34 +137,12 @@ int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t d
       !workspace)
     return DSDE_INVALID_ARG;
   if (N > 0 && (!draft_logits || !draft_tokens || !u_acc || !kld)) return DSDE_INVALID_ARG;
-  if (W < 1 || n_short < 1 || n_short > n_long) return DSDE_INVALID_ARG;
-  if (!(delta > 0.0f && delta <= 1.0f) || !(eps >= 0.0f) || !isfinite(eps)) return DSDE_INVALID_ARG;
-  if (!hist || !head || !count || !mu_last || !var_short || !var_long || !wvir || !sf) return DSDE_INVALID_ARG;
-  if (!isfinite(sl_min) || ceilf(sl_min) > float(sl_hi)) return DSDE_INVALID_ARG;
-  if (!sl_max || !sl_hat || !sl_cap || !sl_next) return DSDE_INVALID_ARG;
+  dsde::SignalArgs sg;
+  const int32_t sst = signal_args(hist, head, count, W, n_short, n_long, delta, eps, mu_last, var_short, var_long,
+                                  wvir, sf, sl_max, sl_min, sl_hi, budget, sl_hat, sl_cap, sl_next, &sg);
+  if (sst != DSDE_OK) return sst;
   if (workspace_bytes < dsde::workspace_layout(B, N, V, k_max).total) return DSDE_WORKSPACE_TOO_SMALL;
   if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return DSDE_INVALID_ARG;
-  dsde::SignalArgs sg;
-  sg.hist = hist;
-  sg.head = head;
-  sg.count = count;
-  sg.W = W;
-  sg.n_short = n_short;
-  sg.n_long = n_long;
-  sg.delta = delta;
-  sg.eps = eps;
-  sg.mu_last = mu_last;
-  sg.var_short = var_short;
-  sg.var_long = var_long;
-  sg.wvir = wvir;
-  sg.sf = sf;
-  sg.sl_max = sl_max;
-  sg.sl_min = sl_min;
-  sg.sl_hi = sl_hi;
-  sg.budget = budget;
-  sg.sl_hat = sl_hat;
-  sg.sl_cap = sl_cap;
-  sg.sl_next = sl_next;
   dsde::VerifyArgs a;
   a.target = target_logits;
   a.draft = draft_logits;
@@ -277,7 +288,28 @@ int32_t dsde_shard_accept(int32_t G, const dsde_shard_partial *parts, int64_t V,
   if (!sl || !cu_sl || !temperature || !u_res || !accepted || !tokens || !jobs || !seq_err) return DSDE_INVALID_ARG;
   if (N > 0 && (!parts || !draft_tokens || !u_acc || !kld)) return DSDE_INVALID_ARG;
   return dsde::launch_shard_accept(G, parts, V, B, N, k_max, sl, cu_sl, draft_tokens, temperature, u_acc, u_res,
-                                   pad_id, accepted, tokens, kld, row_lse, draft_entropy, jobs, seq_err,
+                                   pad_id, accepted, tokens, kld, row_lse, draft_entropy, jobs, seq_err, nullptr,
+                                   static_cast<hipStream_t>(stream));
+}
+
+int32_t dsde_shard_accept_step(int32_t G, const dsde_shard_partial *parts, int64_t V, int32_t B, int64_t N,
+                               int32_t k_max, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
+                               const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
+                               int32_t *accepted, int32_t *tokens, float *kld, double *row_lse,
+                               float *draft_entropy, dsde_draw_job *jobs, float *hist, int32_t *head, int32_t *count,
+                               int32_t W, int32_t n_short, int32_t n_long, float delta, float eps, float *mu_last,
+                               float *var_short, float *var_long, float *wvir, float *sf, const float *sl_max,
+                               float sl_min, int32_t sl_hi, const int32_t *budget, float *sl_hat, float *sl_cap,
+                               int32_t *sl_next, uint32_t *seq_err, void *stream) {
+  if (G < 1 || G > 1024 || !verify_sizes_ok(B, N, V, k_max)) return DSDE_INVALID_ARG;
+  if (!sl || !cu_sl || !temperature || !u_res || !accepted || !tokens || !jobs || !seq_err) return DSDE_INVALID_ARG;
+  if (N > 0 && (!parts || !draft_tokens || !u_acc || !kld)) return DSDE_INVALID_ARG;
+  dsde::SignalArgs sg;
+  const int32_t sst = signal_args(hist, head, count, W, n_short, n_long, delta, eps, mu_last, var_short, var_long,
+                                  wvir, sf, sl_max, sl_min, sl_hi, budget, sl_hat, sl_cap, sl_next, &sg);
+  if (sst != DSDE_OK) return sst;
+  return dsde::launch_shard_accept(G, parts, V, B, N, k_max, sl, cu_sl, draft_tokens, temperature, u_acc, u_res,
+                                   pad_id, accepted, tokens, kld, row_lse, draft_entropy, jobs, seq_err, &sg,
                                    static_cast<hipStream_t>(stream));
 }
 

@@ -10,7 +10,10 @@
 //           partial.
 //   call 2  shard_accept_kernel: one wavefront per sequence folds the G slice
 //           partials in shard order (fp64), then KLD, acceptance and the draw
-//           job exactly as the per-sequence kernel of dsde_verify.
+//           job exactly as the per-sequence kernel of dsde_verify; fused
+//           (dsde_shard_accept_step), the same wavefront then runs the signal
+//           update on those KLD values, and the SL rule follows as in
+//           dsde_step.
 //   call 3  shard_mass_kernel: one workgroup per sequence streams the draw
 //           row(s) of its slice once, keeps chunk and sub-block totals in the
 //           workspace and reports the slice's mass.
@@ -95,13 +98,14 @@ __global__ __launch_bounds__(kShardThreads) void shard_combine_kernel(
 // ---- call 2 --------------------------------------------------------------
 
 // One wavefront per sequence; lane j holds drafted position j.
+template <bool FUSED>
 __global__ __launch_bounds__(64) void shard_accept_kernel(
     int32_t G, const dsde_shard_partial *__restrict__ parts, int64_t N, int64_t V, int32_t k_max,
     const int32_t *__restrict__ sl, const int32_t *__restrict__ cu_sl, const int32_t *__restrict__ draft_tokens,
     const float *__restrict__ temperature, const float *__restrict__ u_acc, const float *__restrict__ u_res,
     int32_t pad_id, int32_t *__restrict__ accepted, int32_t *__restrict__ tokens, float *__restrict__ kld,
     double *__restrict__ row_lse, float *__restrict__ entropy, DrawJob *__restrict__ jobs,
-    uint32_t *__restrict__ seq_err) {
+    uint32_t *__restrict__ seq_err, const SignalArgs S) {
   const int lane = threadIdx.x;
   const int32_t b = blockIdx.x;
   const int32_t width = k_max + 1;
@@ -114,11 +118,14 @@ __global__ __launch_bounds__(64) void shard_accept_kernel(
       DrawJob j{};
       j.kind = -1;
       jobs[b] = j;
+      if constexpr (FUSED) S.mu_last[b] = S.var_short[b] = S.var_long[b] = S.wvir[b] = S.sf[b] = NAN;
     }
     return;
   }
   const int32_t s = sl[b], first = cu_sl[b];
   const float T = temperature[b], ur = u_res[b];
+  RingPrefetch rp{};  // the ring state, in flight while the slices are folded
+  if constexpr (FUSED) rp = wave_ring_prefetch(S.hist + int64_t(b) * S.W, S.head + b, S.count + b, S.W);
   const bool greedy = T == 0.0f;
   int32_t x = 0;
   float u = 0.f;
@@ -210,13 +217,21 @@ __global__ __launch_bounds__(64) void shard_accept_kernel(
       row_lse[2 * (first + lane) + 1] = (double(md) + l2sq) * kLn2;
     }
   }
+  // fused: the signal update of the sequence on the KLD values just formed;
+  // its error bits join seq_err but, as in the separate calls, leave the
+  // acceptance and the draw alone
+  uint32_t e_sig = 0;
+  if constexpr (FUSED)
+    e_sig = wave_signal_update(s, first, nullptr, my_kld, rp, S.hist + int64_t(b) * S.W, S.head + b, S.count + b,
+                               S.W, S.n_short, S.n_long, S.delta, S.eps, S.mu_last + b, S.var_short + b,
+                               S.var_long + b, S.wvir + b, S.sf + b);
   if (lane < width) tok[lane] = lane < acc ? x : pad_id;
   const float a_mt = lanes::readlane(mt, acc), a_md = lanes::readlane(md, acc);
   const float a_isp = lanes::readlane(my_isp, acc), a_isq = lanes::readlane(my_isq, acc);
   const int32_t a_arg = lanes::readlane(abest, acc);
   if (lane == 0) {
     accepted[b] = acc;
-    seq_err[b] = err;
+    seq_err[b] = err | e_sig;
     DrawJob j{};
     j.kind = -1;
     j.accepted = acc;
@@ -578,12 +593,22 @@ int launch_shard_accept(int32_t G, const dsde_shard_partial *parts, int64_t V, i
                         const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
                         const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
                         int32_t *accepted, int32_t *tokens, float *kld, double *row_lse, float *draft_entropy,
-                        dsde_draw_job *jobs, uint32_t *seq_err, hipStream_t stream) {
+                        dsde_draw_job *jobs, uint32_t *seq_err, const SignalArgs *signal, hipStream_t stream) {
   (void)hipGetLastError();
-  shard_accept_kernel<<<dim3(unsigned(B)), dim3(64), 0, stream>>>(
+  DrawJob *dj = reinterpret_cast<DrawJob *>(jobs);
+  if (!signal) {
+    shard_accept_kernel<false><<<dim3(unsigned(B)), dim3(64), 0, stream>>>(
+        G, parts, N, V, k_max, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, pad_id, accepted, tokens, kld,
+        row_lse, draft_entropy, dj, seq_err, SignalArgs{});
+    return hipGetLastError() == hipSuccess ? DSDE_OK : DSDE_DEVICE_ERROR;
+  }
+  const SignalArgs &S = *signal;
+  shard_accept_kernel<true><<<dim3(unsigned(B)), dim3(64), 0, stream>>>(
       G, parts, N, V, k_max, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, pad_id, accepted, tokens, kld,
-      row_lse, draft_entropy, reinterpret_cast<DrawJob *>(jobs), seq_err);
-  return hipGetLastError() == hipSuccess ? DSDE_OK : DSDE_DEVICE_ERROR;
+      row_lse, draft_entropy, dj, seq_err, S);
+  if (hipGetLastError() != hipSuccess) return DSDE_DEVICE_ERROR;
+  return launch_next_sl(B, S.sf, S.wvir, S.sl_max, S.sl_min, S.sl_hi, S.budget, S.sl_hat, S.sl_cap, S.sl_next,
+                        seq_err, true, stream);
 }
 
 int launch_shard_draw_mass(const ShardRows &r, const dsde_shard_partial *part, const dsde_draw_job *jobs,

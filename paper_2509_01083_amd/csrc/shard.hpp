@@ -49,7 +49,7 @@ int launch_shard_accept(int32_t G, const dsde_shard_partial *parts, int64_t V, i
                         const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
                         const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
                         int32_t *accepted, int32_t *tokens, float *kld, double *row_lse, float *draft_entropy,
-                        dsde_draw_job *jobs, uint32_t *seq_err, hipStream_t stream);
+                        dsde_draw_job *jobs, uint32_t *seq_err, const SignalArgs *signal, hipStream_t stream);
 int launch_shard_draw_mass(const ShardRows &r, const dsde_shard_partial *part, const dsde_draw_job *jobs,
                            dsde_shard_mass *mass);
 int launch_shard_draw_pick(const ShardRows &r, int32_t G, int32_t g, const dsde_shard_mass *masses,

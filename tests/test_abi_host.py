@@ -204,6 +204,23 @@ def test_shard_accept_rejects_invalid_arguments(lib, over):
 
 
 @pytest.mark.parametrize("over", [
+    dict(G=0), dict(B=0), dict(parts=None), dict(jobs=None), dict(err=None), dict(W=0), dict(n_short=0),
+    dict(n_short=31), dict(delta=0.0), dict(delta=1.5), dict(eps=-1.0), dict(hist=None), dict(sf=None),
+    dict(sl_max=None), dict(sl_min=float("nan")), dict(sl_min=9.0), dict(sl_next=None),
+])
+def test_shard_accept_step_rejects_invalid_arguments(lib, over):
+    """The fused call 2 checks call 2's arguments and the signal and SL-rule
+    arguments of dsde_step before anything is enqueued."""
+    a = dict(G=2, parts=FAKE, V=1000, B=4, N=8, k_max=4, sl=FAKE, cu_sl=FAKE, toks=FAKE, temp=FAKE, u_acc=FAKE,
+             u_res=FAKE, pad=-1, acc=FAKE, tokens=FAKE, kld=FAKE, lse=None, ent=None, jobs=FAKE,
+             hist=FAKE, head=FAKE, count=FAKE, W=32, n_short=10, n_long=30, delta=0.85, eps=1e-6,
+             mu_last=FAKE, var_short=FAKE, var_long=FAKE, wvir=FAKE, sf=FAKE, sl_max=FAKE, sl_min=2.0, sl_hi=8,
+             budget=None, sl_hat=FAKE, sl_cap=FAKE, sl_next=FAKE, err=FAKE, stream=None)
+    a.update(over)
+    assert lib.dsde_shard_accept_step(*a.values()) == 1
+
+
+@pytest.mark.parametrize("over", [
     dict(dtype=2), dict(V_shard=0), dict(v_begin=-1), dict(B=0), dict(target=None), dict(draft=None),
     dict(part=None), dict(jobs=None), dict(mass=None), dict(ws=None),
 ])

@@ -168,3 +168,48 @@ def test_sharded_equals_unsharded_on_kld(gpu_lib):
     assert np.array_equal(whole["seq_err"], split["seq_err"])
     d = np.abs(whole["kld"].astype(np.float64) - split["kld"].astype(np.float64))
     assert (d <= 1e-4 * np.abs(whole["kld"]) + 1e-6).all(), d.max()
+
+
+@pytest.mark.parametrize("name", ["b256", "greedy", "layout"])
+def test_fused_shard_acceptance_equals_the_three_calls(gpu_lib, name):
+    """dsde_shard_accept_step against dsde_shard_accept, dsde_kld_signal and
+    dsde_next_sl in turn, from the same gathered partials: identical bits (the
+    layout case breaks cu_sl: every sequence flagged, the SL rule still runs)."""
+    import paper_2509_01083_amd as dsde
+    cfg = W.CONFIGS["b64" if name == "layout" else name]
+    step = W.make_step(cfg, seed=17, device="cuda")
+    if name == "layout":
+        cu = step.cu_sl.clone()
+        cu[1] += 1
+        step = W.Step(**{**step.__dict__, "cu_sl": cu})
+    announce(f"fused shard acceptance {name}")
+    base = dsde.verify_sharded(step.target, step.draft, step.sl, step.cu_sl, step.draft_tokens, step.temperature,
+                               step.u_acc, step.u_res, step.k_max, dsde.slice_bounds(step.V, 4))
+    parts, err0 = base["parts"], base["shard_seq_err"][0]
+    st = W.make_signal_state(cfg, seed=17, device="cuda")
+    st_a = W.SignalState(hist=st.hist.clone(), head=st.head.clone(), count=st.count.clone(), sl_max=st.sl_max)
+    st_b = W.SignalState(hist=st.hist.clone(), head=st.head.clone(), count=st.count.clone(), sl_max=st.sl_max)
+    budget = torch.as_tensor(np.random.default_rng(5).integers(0, 10, step.B).astype(np.int32), device="cuda")
+    args = (parts, step.V, step.sl, step.cu_sl, step.draft_tokens, step.temperature, step.u_acc, step.u_res,
+            step.k_max)
+    e_a = err0.clone()
+    a = dsde.shard_accept(*args, e_a, draft_entropy=True)
+    s_ = dsde.kld_signal(step.sl, step.cu_sl, a["kld"], st_a.hist, st_a.head, st_a.count)
+    n_ = dsde.next_sl(s_["sf"], s_["wvir"], st_a.sl_max, 2.0, step.k_max, budget=budget)
+    e_b = err0.clone()
+    f = dsde.shard_accept_step(*args, e_b, st_b.hist, st_b.head, st_b.count, st_b.sl_max, draft_entropy=True,
+                               budget=budget)
+    torch.cuda.synchronize()
+    chain = {**a, **s_, **n_}
+    for k in ("accepted", "tokens", "jobs", "sl_next"):
+        assert torch.equal(chain[k], f[k]), k
+    written = ("mu_last", "var_short", "var_long", "wvir", "sf", "sl_hat", "sl_cap")
+    if name != "layout":  # the KLD is not written under an invalid layout
+        written = ("kld", "draft_entropy") + written
+    for k in written:
+        assert torch.equal(chain[k].view(torch.int32), f[k].view(torch.int32)), k
+    assert torch.equal(st_a.hist.view(torch.int32), st_b.hist.view(torch.int32))
+    assert torch.equal(st_a.head, st_b.head) and torch.equal(st_a.count, st_b.count)
+    assert torch.equal(e_a | s_["seq_err"] | n_["seq_err"], e_b)
+    if name == "layout":
+        assert (e_b.cpu().numpy() & 1).all()
