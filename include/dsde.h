@@ -271,7 +271,8 @@ int32_t dsde_calibrate_sl_max(int32_t B, const int32_t *a_max, const double *kld
  * the sums split at slice boundaries: accepted counts, tokens and error bits
  * outside the tie bands, KLD within the same tolerance.  dsde_kld_signal and
  * dsde_next_sl then run unchanged on every shard (their inputs are identical
- * there).  Every pointer, layout and error rule of dsde_verify applies; the
+ * there), or fused behind call 2 (dsde_shard_accept_step).  Every pointer,
+ * layout and error rule of dsde_verify applies; the
  * calls of one shard share its workspace (dsde_shard_workspace_bytes), whose
  * contents pass from call 1 to 2 (none), 3 to 4 (the slice's chunk totals).
  */
