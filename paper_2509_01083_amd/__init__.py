@@ -376,7 +376,7 @@ def shard_stats(target, draft, v_begin, V, sl, cu_sl, draft_tokens, temperature,
 
 
 def _shard_accept_call(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, seq_err, pad_id,
-                       row_lse, draft_entropy, out):
+                       row_lse, draft_entropy, out, stream):
     """Output buffers and the leading ctypes arguments shared by the two call-2 entry points."""
     G = int(parts.shape[0])
     B = int(sl.shape[0])
@@ -394,7 +394,9 @@ def _shard_accept_call(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_
         out["draft_entropy"] = torch.empty(max(N, 1), dtype=torch.float32, device=dev)[:N]
     ent = out.get("draft_entropy") if draft_entropy else None
     if N > 0 and int(parts.shape[1]) != N:
-        parts = parts[:, :N].contiguous()
+        # the packed copy is made on the call's stream, ahead of the call
+        with torch.cuda.stream(stream if stream is not None else torch.cuda.current_stream()):
+            parts = parts[:, :N].contiguous()
     args = [G, _ptr(parts, torch.uint8, G * N * SHARD_PARTIAL_BYTES, "parts") if N > 0 else None, int(V), B, N,
             k_max, _ptr(sl, torch.int32, B, "sl"), _ptr(cu_sl, torch.int32, B + 1, "cu_sl"),
             _ptr(draft_tokens, torch.int32, N, "draft_tokens") if N > 0 else None,
@@ -416,7 +418,7 @@ def shard_accept(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k
     with accepted, tokens, kld, seq_err, jobs [B, 44] uint8 (and draft_entropy)."""
     lib = load()
     out, args, _keep = _shard_accept_call(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max,
-                                          seq_err, pad_id, row_lse, draft_entropy, out)
+                                          seq_err, pad_id, row_lse, draft_entropy, out, stream)
     B = int(sl.shape[0])
     _check(lib.dsde_shard_accept(*args, _ptr(seq_err, None, B, "seq_err"), _stream(stream)))
     return out
@@ -431,7 +433,7 @@ def shard_accept_step(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_r
     sl_next."""
     lib = load()
     out, args, _keep = _shard_accept_call(parts, V, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max,
-                                          seq_err, pad_id, row_lse, draft_entropy, out)
+                                          seq_err, pad_id, row_lse, draft_entropy, out, stream)
     B = int(sl.shape[0])
     W = int(hist.shape[1])
     sl_hi = k_max if sl_hi is None else sl_hi
