@@ -53,6 +53,10 @@ CONFIGS = {
                    prefill=True),
     "b256g": dict(B=256, sl=("uniform", 1, 8), V=128256, dtype="bf16", sigma_z=4.0, zipf=1.05,
                   draft=("noise", 0.2, 4.0), temp=("all", 0.0), W=32, sl_max=8.0, k_max=8, prefill=True),
+    # one GPU's share of b256 with the batch split eight ways (32 sequences)
+    "batch8": dict(B=32, sl=("uniform", 1, 8), V=128256, dtype="bf16", sigma_z=4.0, zipf=1.05,
+                   draft=("noise", 0.2, 4.0), temp=("alternate", 0.7, 1.0), W=32, sl_max=8.0, k_max=8,
+                   prefill=True),
     "loop": dict(B=1024, sl=("uniform", 2, 8), V=128256, dtype="bf16", sigma_z=4.0, zipf=1.05,
                  draft=("walk", 0.2, 4.0), temp=("all", 1.0), W=32, sl_max=8.0, k_max=8, prefill=False,
                  steps=200),
