@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define DSDE_ABI_VERSION 2
+#define DSDE_ABI_VERSION 3
 
 /* status codes */
 #define DSDE_OK 0
@@ -150,8 +150,12 @@ int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t
  * n_s = min(n_short, count) and n_l = min(n_long, count) newest entries h_1..h_n
  * (h_1 newest) with weights alpha_i = delta^(i-1):
  *   mu_w = sum alpha_i h_i / sum alpha_i,  Var_w = sum alpha_i (h_i - mu_w)^2 / sum alpha_i
- *   WVIR = Var_s / (Var_l + eps),          SF = exp(2 mu_last) - 1.
- * An empty window has variance 0.
+ *   WVIR = Var_s / Var_l (Eq. 4),          SF = exp(2 mu_last) - 1.
+ * The sums are taken over h_i - h_1 (Var_w does not change under a common
+ * shift), so a window of equal entries has a variance of exactly 0.  Where
+ * Var_l = 0 (the long window holds one value; its short window is constant
+ * too) eps replaces it in the quotient, giving WVIR = 0.  An empty window
+ * has variance 0.
  *
  *   B, N                     sequences and drafted positions (as in dsde_verify)
  *   sl [B], cu_sl [B+1]      int32   as in dsde_verify
@@ -161,7 +165,7 @@ int32_t dsde_verify(const void *target_logits, const void *draft_logits, int32_t
  *   W                                ring capacity (>= 1)
  *   n_short, n_long                  window sizes, 1 <= n_short <= n_long (paper: 10, 30)
  *   delta                            recency decay in (0, 1] (paper: 0.85)
- *   eps                              >= 0, added to Var_l (1e-6)
+ *   eps                              > 0 and finite: divisor of WVIR where Var_l = 0 (1e-6)
  * Outputs [B] float: mu_last, var_short, var_long, wvir, sf; seq_err [B] uint32
  * (DSDE_ERR_LAYOUT, DSDE_ERR_SIGNAL, DSDE_ERR_STATE; a flagged ring is left unchanged).
  */

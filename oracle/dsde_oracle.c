@@ -49,7 +49,8 @@
  *     one history entry per (sequence, step); the entry is pushed before the
  *     windows are taken, so i = 1 is the step just verified.
  *   - Window sizes are min(n_short, count) and min(n_long, count); an empty
- *     window has mean 0 and variance 0; WVIR = Var_s / (Var_l + eps).
+ *     window has mean 0 and variance 0; WVIR = Var_s / Var_l (Eq. 4), with
+ *     eps > 0 in place of Var_l only when Var_l = 0 (then WVIR = 0).
  *   - Acceptance is strict (u < min(1, r)); the inverse-CDF draw walks token
  *     ids in ascending order and returns the smallest id whose cumulative
  *     weight exceeds u' * Z.
@@ -386,27 +387,31 @@ int oracle_verify(const void *target, const void *draft, int32_t dtype, int64_t 
 /* ------------------------------------------------------------------ */
 
 /* Weighted mean and population variance (Eqs. 5-7) of the n newest entries
- * h_1..h_n (h_1 newest) with alpha_i = delta^(i-1). */
+ * h_1..h_n (h_1 newest) with alpha_i = delta^(i-1).  The sums run over the
+ * entries less h_1: a common shift leaves Eq. 7 unchanged, and with it a
+ * window of equal entries has a variance of exactly 0 instead of a rounding
+ * residue of its mean. */
 static void weighted_stats(const double *newest_first, int32_t n, double delta, double *mean, double *var) {
   if (n <= 0) {
     *mean = 0.0;
     *var = 0.0;
     return;
   }
-  double sa = 0.0, sah = 0.0;
+  const double h1 = newest_first[0];
+  double sa = 0.0, sad = 0.0;
   for (int32_t i = 1; i <= n; ++i) {
     double alpha = pow(delta, (double)(i - 1));
     sa += alpha;
-    sah += alpha * newest_first[i - 1];
+    sad += alpha * (newest_first[i - 1] - h1);
   }
-  double mu = sah / sa;
+  double mu_d = sad / sa; /* the weighted mean less h_1 */
   double sv = 0.0;
   for (int32_t i = 1; i <= n; ++i) {
     double alpha = pow(delta, (double)(i - 1));
-    double d = newest_first[i - 1] - mu;
+    double d = (newest_first[i - 1] - h1) - mu_d;
     sv += alpha * d * d;
   }
-  *mean = mu;
+  *mean = h1 + mu_d;
   *var = sv / sa;
 }
 
@@ -421,7 +426,10 @@ static void signal_from_history(const double *newest_first, int32_t count, doubl
   double ms, ml;
   weighted_stats(newest_first, ns, delta, &ms, var_s);
   weighted_stats(newest_first, nl, delta, &ml, var_l);
-  *wvir = *var_s / (*var_l + eps);
+  /* Eq. 4 as printed; eps stands in for the long-window variance only where
+   * that is 0 (a window of equal entries, whose short window is constant
+   * too, so WVIR = 0) */
+  *wvir = *var_s / (*var_l > 0.0 ? *var_l : eps);
   *sf = exp(2.0 * mu_last) - 1.0;
 }
 
@@ -430,7 +438,7 @@ int oracle_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu
                       double delta, double eps, double *mu_last, double *var_short, double *var_long,
                       double *wvir, double *sf, uint32_t *seq_err) {
   if (B < 1 || N < 0 || W < 1 || n_short < 1 || n_short > n_long || !(delta > 0.0 && delta <= 1.0) ||
-      !(eps >= 0.0))
+      !(eps > 0.0))
     return 1;
   int layout_ok = cu_sl[0] == 0 && (int64_t)cu_sl[B] == N;
   for (int32_t b = 0; b < B && layout_ok; ++b)

@@ -95,7 +95,7 @@ static int32_t signal_args(float *hist, int32_t *head, int32_t *count, int32_t W
                            float *sf, const float *sl_max, float sl_min, int32_t sl_hi, const int32_t *budget,
                            float *sl_hat, float *sl_cap, int32_t *sl_next, dsde::SignalArgs *sg) {
   if (W < 1 || n_short < 1 || n_short > n_long) return DSDE_INVALID_ARG;
-  if (!(delta > 0.0f && delta <= 1.0f) || !(eps >= 0.0f) || !isfinite(eps)) return DSDE_INVALID_ARG;
+  if (!(delta > 0.0f && delta <= 1.0f) || !(eps > 0.0f) || !isfinite(eps)) return DSDE_INVALID_ARG;
   if (!hist || !head || !count || !mu_last || !var_short || !var_long || !wvir || !sf) return DSDE_INVALID_ARG;
   if (!isfinite(sl_min) || ceilf(sl_min) > float(sl_hi)) return DSDE_INVALID_ARG;
   if (!sl_max || !sl_hat || !sl_cap || !sl_next) return DSDE_INVALID_ARG;
@@ -177,7 +177,7 @@ int32_t dsde_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *
                         int32_t n_long, float delta, float eps, float *mu_last, float *var_short,
                         float *var_long, float *wvir, float *sf, uint32_t *seq_err, void *stream) {
   if (B < 1 || N < 0 || W < 1 || n_short < 1 || n_short > n_long) return DSDE_INVALID_ARG;
-  if (!(delta > 0.0f && delta <= 1.0f) || !(eps >= 0.0f) || !isfinite(eps)) return DSDE_INVALID_ARG;
+  if (!(delta > 0.0f && delta <= 1.0f) || !(eps > 0.0f) || !isfinite(eps)) return DSDE_INVALID_ARG;
   if (!sl || !cu_sl || !hist || !head || !count || !mu_last || !var_short || !var_long || !wvir || !sf ||
       !seq_err)
     return DSDE_INVALID_ARG;

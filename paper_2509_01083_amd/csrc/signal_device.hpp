@@ -71,7 +71,10 @@ __device__ __forceinline__ double pow_int(double x, int32_t n) {
 // Recency-weighted means and population variances (Eqs. 6-7) of the ns and
 // nl newest ring entries (ns <= nl), evaluated together by one wavefront:
 // entry i (i = 0 newest, value h1 passed in registers) sits in ring slot
-// (newest - i) mod W and has weight alpha = delta^i.  Lane l holds entries
+// (newest - i) mod W and has weight alpha = delta^i.  The sums take each
+// entry less h1 (exact in double: both are floats), which leaves Eq. 7
+// unchanged and gives a window of equal entries a variance of exactly 0.  The
+// means returned are those of the entries less h1.  Lane l holds entries
 // l, l + 64, ...; fixed-order sums, bitwise reproducible.
 __device__ inline void wave_windows(const RingPrefetch &rp, const float *ring, int32_t W, int32_t newest, float h1,
                                     int32_t ns, int32_t nl, double delta, double *ms, double *vs, double *ml,
@@ -84,7 +87,7 @@ __device__ inline void wave_windows(const RingPrefetch &rp, const float *ring, i
     const int32_t slot = i < W ? (newest - i + W) % W : 0;
     const float raw = ring_slot(rp, ring, W, slot);
     if (i < nl) {
-      const double h = i == 0 ? double(h1) : double(raw);
+      const double h = i == 0 ? 0.0 : double(raw) - double(h1);
       const double a = pow_int(delta, i);
       sa_l += a;
       sah_l += a * h;
@@ -105,7 +108,7 @@ __device__ inline void wave_windows(const RingPrefetch &rp, const float *ring, i
     const int32_t slot = i < W ? (newest - i + W) % W : 0;
     const float raw = ring_slot(rp, ring, W, slot);
     if (i < nl) {
-      const double h = i == 0 ? double(h1) : double(raw);
+      const double h = i == 0 ? 0.0 : double(raw) - double(h1);
       const double a = pow_int(delta, i);
       const double dl = h - mu_l;
       sv_l += a * dl * dl;
@@ -179,7 +182,9 @@ __device__ inline uint32_t wave_signal_update(int32_t s, int64_t first, const fl
     *mu_last = float(mu);
     *var_short = float(vs);
     *var_long = float(vl);
-    *wvir = float(vs / (vl + double(eps)));
+    // Eq. 4; eps stands in for the long-window variance only where that is 0
+    // (equal entries, so the short window is constant too and WVIR = 0)
+    *wvir = float(vs / (vl > 0.0 ? vl : double(eps)));
     *sf = float(expm1(2.0 * mu));
   }
   return 0;

@@ -42,7 +42,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.dsde_abi_version() == 2
+    assert lib.dsde_abi_version() == 3
     for code, text in ((0, b"ok"), (1, b"invalid argument"), (2, b"workspace too small"), (3, b"device error")):
         assert lib.dsde_status_string(code) == text
     assert lib.dsde_status_string(99) == b"unknown status"
@@ -99,7 +99,7 @@ def signal_args(**over):
 
 @pytest.mark.parametrize("over", [
     dict(B=0), dict(N=-1), dict(W=0), dict(ns=0), dict(ns=31), dict(delta=0.0), dict(delta=1.5),
-    dict(delta=float("nan")), dict(eps=-1.0), dict(eps=float("inf")), dict(sl=None), dict(hist=None),
+    dict(delta=float("nan")), dict(eps=-1.0), dict(eps=0.0), dict(eps=float("inf")), dict(sl=None), dict(hist=None),
     dict(head=None), dict(count=None), dict(mu=None), dict(sf=None), dict(err=None), dict(kld=None),
 ])
 def test_kld_signal_rejects_invalid_arguments(lib, over):
@@ -205,7 +205,7 @@ def test_shard_accept_rejects_invalid_arguments(lib, over):
 
 @pytest.mark.parametrize("over", [
     dict(G=0), dict(B=0), dict(parts=None), dict(jobs=None), dict(err=None), dict(W=0), dict(n_short=0),
-    dict(n_short=31), dict(delta=0.0), dict(delta=1.5), dict(eps=-1.0), dict(hist=None), dict(sf=None),
+    dict(n_short=31), dict(delta=0.0), dict(delta=1.5), dict(eps=-1.0), dict(eps=0.0), dict(hist=None), dict(sf=None),
     dict(sl_max=None), dict(sl_min=float("nan")), dict(sl_min=9.0), dict(sl_next=None),
 ])
 def test_shard_accept_step_rejects_invalid_arguments(lib, over):

@@ -28,6 +28,9 @@ MUTANTS = {
     "bessel_variance": ("*var = sv / sa;", "*var = sv / (sa - 1.0);"),
     "weights_reversed": ("double alpha = pow(delta, (double)(i - 1));\n    sa += alpha;",
                          "double alpha = pow(delta, (double)(n - i));\n    sa += alpha;"),
+    "wvir_guard_always_added": ("*wvir = *var_s / (*var_l > 0.0 ? *var_l : eps);",
+                                "*wvir = *var_s / (*var_l + eps);"),
+    "window_not_shifted": ("sad += alpha * (newest_first[i - 1] - h1);", "sad += alpha * newest_first[i - 1];"),
     "scale_factor": ("*sf = exp(2.0 * mu_last) - 1.0;", "*sf = exp(mu_last) - 1.0;"),
     "cap_not_mean": ("double cap = n > 0 ? sum / (double)n : NAN;",
                      "double cap = n > 0 ? sum / (double)(n + 1) : NAN;"),

@@ -386,7 +386,29 @@ def test_wvir_is_ratio_of_window_variances(orc):
     rng = np.random.default_rng(13)
     vals = list(rng.random(31))
     out = _signal_one(orc, vals[:-1], 32, [vals[-1]])
-    assert out["wvir"][0] == pytest.approx(out["var_short"][0] / (out["var_long"][0] + 1e-6), rel=1e-14)
+    assert out["wvir"][0] == pytest.approx(out["var_short"][0] / out["var_long"][0], rel=1e-14)
+
+
+def test_wvir_small_variances_closed_form(orc):
+    """Eq. 4 has no guard term: with window variances near 1e-6 WVIR is still
+    their plain ratio.  Newest first a, a + 2e-3, a - 1e-3 with delta = 1 and
+    windows of 2 and 3: Var_s = (2e-3)^2 / 4 = 1e-6 and Var_l = 42/27 * 1e-6
+    (population variance of 0, 2e-3, -1e-3), so WVIR = 27/42."""
+    a = 0.1
+    out = _signal_one(orc, [a - 1e-3, a + 2e-3], 8, [a], delta=1.0, n_short=2, n_long=3)
+    assert out["var_short"][0] == pytest.approx(1e-6, rel=1e-9)
+    assert out["var_long"][0] == pytest.approx(42.0 / 27.0 * 1e-6, rel=1e-9)
+    assert out["wvir"][0] == pytest.approx(27.0 / 42.0, rel=1e-9)
+
+
+def test_wvir_constant_window_is_zero_and_eps_must_be_positive(orc):
+    # a constant long window (and so a constant short one): variances exactly 0, WVIR = 0
+    out = _signal_one(orc, [0.3] * 40, 32, [0.3])
+    assert out["var_short"][0] == 0.0 and out["var_long"][0] == 0.0 and out["wvir"][0] == 0.0
+    h, head, cnt = _ring([0.3] * 8, 8)
+    sl, cu = packed_layout([1])
+    with pytest.raises(ValueError):
+        orc.kld_signal(sl, cu, np.array([0.3]), h[None, :], [head], [cnt], eps=0.0)
 
 
 # ---------------------------------------------------------------- SL rule and cap
