@@ -153,12 +153,18 @@ __device__ __forceinline__ RawBf16 load_raw_bf16(const void *row, int64_t V, int
   return r;
 }
 
-__device__ __forceinline__ float max2(uint32_t w) { return fmaxf(bf_lo(w), bf_hi(w)); }
+// Larger of two floats, NaN if either is NaN (the IEEE 754-2019 maximum:
+// v_maximum3_f32 on gfx950).  fmaxf would first quiet every loaded value
+// (one v_max_f32 x, x, x per logit in IEEE mode).  A NaN logit makes its
+// chunk maximum NaN, and with it every sum of the chunk, so the row is
+// flagged as with fmaxf.
+__device__ __forceinline__ float max_nan(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float max2(uint32_t w) { return max_nan(bf_lo(w), bf_hi(w)); }
 __device__ __forceinline__ float vmax(uint4 v) {
-  return fmaxf(fmaxf(max2(v.x), max2(v.y)), fmaxf(max2(v.z), max2(v.w)));
+  return max_nan(max_nan(max2(v.x), max2(v.y)), max_nan(max2(v.z), max2(v.w)));
 }
 __device__ __forceinline__ float raw_max(const RawBf16 &r) {
-  return fmaxf(fmaxf(vmax(r.v0), vmax(r.v1)), fmaxf(vmax(r.v2), vmax(r.v3)));
+  return max_nan(max_nan(vmax(r.v0), vmax(r.v1)), max_nan(vmax(r.v2), vmax(r.v3)));
 }
 __device__ __forceinline__ float pick_bf16(const RawBf16 &r, int i) {
   const uint4 v = (i >> 3) == 0 ? r.v0 : (i >> 3) == 1 ? r.v1 : (i >> 3) == 2 ? r.v2 : r.v3;
@@ -167,24 +173,40 @@ __device__ __forceinline__ float pick_bf16(const RawBf16 &r, int i) {
   return (i & 1) ? bf_hi(x) : bf_lo(x);
 }
 
-// Statistics of one logit pair with references rt, rd (log2 domain): the two
-// exponential sums, the KL accumulator sum 2^at (at - ad), and the draft
-// entropy accumulator sum 2^ad ad.
-__device__ __forceinline__ void acc_pair(float zt, float zd, float c, float rt, float rd, float &sp, float &sq,
-                                         float &a, float &h) {
+// Per-thread accumulators of the statistics pass, two interleaved sets
+// (index 0 and 1).  The exponential sums are fp64: near-identical target and
+// draft rows make KL = A / S_p - log S_p + log S_q cancel to values of order
+// 1e-4 and below, and a thread's fp32 running sum near 1 (its largest
+// exponential is 1 at the chunk maximum) would round each later term to
+// about 6e-8 of it, leaving ~1e-7 of uncorrelated relative error in S_p and
+// S_q; summing the fp32 exponentials in fp64 leaves only their own rounding.
+// The KL and entropy accumulators enter the results through ratios to the
+// sums and stay fp32.
+struct PairAcc {
+  double sp[2], sq[2];  // sum 2^at, sum 2^ad
+  float a[2], h[2];     // sum 2^at (at - ad), sum 2^ad ad
+};
+__device__ __forceinline__ void zero(PairAcc &s) {
+  s.sp[0] = s.sp[1] = s.sq[0] = s.sq[1] = 0.0;
+  s.a[0] = s.a[1] = s.h[0] = s.h[1] = 0.0f;
+}
+
+// Statistics of one logit pair with references rt, rd (log2 domain) into
+// accumulator set k: the two exponential sums, the KL accumulator
+// sum 2^at (at - ad), and the draft entropy accumulator sum 2^ad ad.
+__device__ __forceinline__ void acc_pair(float zt, float zd, float c, float rt, float rd, PairAcc &s, int k) {
   const float at = fmaf(zt, c, -rt), ad = fmaf(zd, c, -rd);
   const float et = fast_exp2(at), ed = fast_exp2(ad);
-  sp += et;
-  sq += ed;
-  a = fmaf(et, at - ad, a);
-  h = fmaf(ed, ad, h);
+  s.sp[k] += double(et);
+  s.sq[k] += double(ed);
+  s.a[k] = fmaf(et, at - ad, s.a[k]);
+  s.h[k] = fmaf(ed, ad, s.h[k]);
 }
-// Two interleaved accumulator sets: s[0..3] and s[4..7].
-__device__ __forceinline__ void acc_word(uint32_t t, uint32_t d, float c, float rt, float rd, float (&s)[8]) {
-  acc_pair(bf_lo(t), bf_lo(d), c, rt, rd, s[0], s[1], s[2], s[3]);
-  acc_pair(bf_hi(t), bf_hi(d), c, rt, rd, s[4], s[5], s[6], s[7]);
+__device__ __forceinline__ void acc_word(uint32_t t, uint32_t d, float c, float rt, float rd, PairAcc &s) {
+  acc_pair(bf_lo(t), bf_lo(d), c, rt, rd, s, 0);
+  acc_pair(bf_hi(t), bf_hi(d), c, rt, rd, s, 1);
 }
-__device__ __forceinline__ void acc_vec(uint4 t, uint4 d, float c, float rt, float rd, float (&s)[8]) {
+__device__ __forceinline__ void acc_vec(uint4 t, uint4 d, float c, float rt, float rd, PairAcc &s) {
   acc_word(t.x, d.x, c, rt, rd, s);
   acc_word(t.y, d.y, c, rt, rd, s);
   acc_word(t.z, d.z, c, rt, rd, s);

@@ -100,24 +100,42 @@ __device__ __forceinline__ void wave_chunk_argmax(float M, float tmax, Z z, int6
   if (lane == 0) red[wave] = best;
 }
 
-// Chunk sums of one workgroup -> one PairChunk (fixed order: lanes, then waves
-// in fp64); with `arg` set (greedy pairs), also the chunk maximum M of the
-// target row and the smallest token holding it, from the per-wave candidates
-// wave_chunk_argmax left in red_arg (the same barrier serves both).
-__device__ __forceinline__ void write_pair_chunk(float rt, float rd, float sp, float sq, float a, float h,
-                                                 float (*red)[kWaves], PairChunk *out, float M,
-                                                 const uint32_t *red_arg, ChunkArg *arg) {
+// Sum over the 64 lanes of a wavefront of four fp64 values at once (a
+// reduce-scatter): lanes whose bits 5 and 4 are (0, 0), (0, 1), (1, 0) and
+// (1, 1) end up holding the totals of v0, v1, v2 and v3.  The first exchange
+// (partner lane ^ 32) keeps v0, v1 in the lower half of the wavefront and
+// v2, v3 in the upper half, the second (lane ^ 16) keeps one of the two, and
+// four butterfly steps finish each group of 16 lanes; every step adds the
+// same two partials on both partners, so a group's lanes agree bit for bit.
+__device__ __forceinline__ double wave_sum4_scatter(double v0, double v1, double v2, double v3) {
+  const int lane = threadIdx.x & 63;
+  const bool up5 = (lane & 32) != 0, up4 = (lane & 16) != 0;
+  const double k0 = up5 ? v2 : v0, k1 = up5 ? v3 : v1;
+  const double g0 = up5 ? v0 : v2, g1 = up5 ? v1 : v3;
+  const double a0 = k0 + __shfl_xor(g0, 32), a1 = k1 + __shfl_xor(g1, 32);
+  const double k = up4 ? a1 : a0, g = up4 ? a0 : a1;
+  double r = k + __shfl_xor(g, 16);
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) r += __shfl_xor(r, o);
+  return r;
+}
+
+// Chunk sums of one workgroup -> one PairChunk.  Each thread's two
+// accumulator sets (the p sum, the q sum, the KL and the entropy
+// accumulators) are joined in fp64, summed over the wavefront in fp64 and
+// over the wavefronts in fp64, in a fixed order.  The fp64 wavefront sums
+// matter for the KLD: KL = A / S_p - log2 S_p + log2 S_q cancels terms of
+// order one down to values of order 1e-4, so rounding the partial sums to
+// fp32 on the way (six butterfly levels) would cost about 1e-7 of absolute
+// KLD accuracy.  With `arg` set (greedy pairs), also the chunk maximum M of
+// the target row and the smallest token holding it, from the per-wave
+// candidates wave_chunk_argmax left in red_arg (the same barrier serves both).
+__device__ __forceinline__ void write_pair_chunk(float rt, float rd, const PairAcc &s, double (*red)[kWaves],
+                                                 PairChunk *out, float M, const uint32_t *red_arg, ChunkArg *arg) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  sp = wave_sum(sp);
-  sq = wave_sum(sq);
-  a = wave_sum(a);
-  h = wave_sum(h);
-  if (lane == 0) {
-    red[2][wave] = sp;
-    red[3][wave] = sq;
-    red[4][wave] = a;
-    red[5][wave] = h;
-  }
+  const double tot = wave_sum4_scatter(s.sp[0] + s.sp[1], s.sq[0] + s.sq[1], double(s.a[0]) + double(s.a[1]),
+                                       double(s.h[0]) + double(s.h[1]));
+  if ((lane & 15) == 0) red[lane >> 4][wave] = tot;
   __syncthreads();
   if (t == 0) {
     PairChunk pc;
@@ -126,10 +144,10 @@ __device__ __forceinline__ void write_pair_chunk(float rt, float rd, float sp, f
     pc.sp = pc.sq = pc.a = pc.h = 0.0;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
-      pc.sp += double(red[2][w]);
-      pc.sq += double(red[3][w]);
-      pc.a += double(red[4][w]);
-      pc.h += double(red[5][w]);
+      pc.sp += red[0][w];
+      pc.sq += red[1][w];
+      pc.a += red[2][w];
+      pc.h += red[3][w];
     }
     *out = pc;
     if (arg) {
@@ -149,7 +167,8 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
                                                              int64_t token_base, PairChunk *__restrict__ out,
                                                              Gathered *__restrict__ gathered,
                                                              ChunkArg *__restrict__ chunk_arg) {
-  __shared__ float red[6][kWaves];
+  __shared__ float red[2][kWaves];
+  __shared__ double red_sum[4][kWaves];
   __shared__ uint32_t red_arg[kWaves];
   const int64_t unit = blockIdx.x;
   const int64_t k = unit / nc;
@@ -171,7 +190,8 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
   if (greedy)
     wave_chunk_argmax<DSDE_BF16, true>(Mt, tmt, [&](int i) { return pick_bf16(rt_, i); }, chunk, red_arg);
   const float rt = Mt * c, rd = Md * c;
-  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  PairAcc s;
+  zero(s);
   acc_vec(rt_.v0, rd_.v0, c, rt, rd, s);
   acc_vec(rt_.v1, rd_.v1, c, rt, rd, s);
   acc_vec(rt_.v2, rd_.v2, c, rt, rd, s);
@@ -196,8 +216,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
       gathered[w.slot] = Gathered{a, b};
     }
   }
-  write_pair_chunk(rt, rd, s[0] + s[4], s[1] + s[5], s[2] + s[6], s[3] + s[7], red,
-                   out + int64_t(w.slot) * nc + chunk, Mt, red_arg,
+  write_pair_chunk(rt, rd, s, red_sum, out + int64_t(w.slot) * nc + chunk, Mt, red_arg,
                    greedy ? chunk_arg + int64_t(w.slot) * nc + chunk : nullptr);
 }
 
@@ -210,7 +229,8 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
                                                                 int64_t token_base, PairChunk *__restrict__ out,
                                                                 Gathered *__restrict__ gathered,
                                                                 ChunkArg *__restrict__ chunk_arg) {
-  __shared__ float red[6][kWaves];
+  __shared__ float red[2][kWaves];
+  __shared__ double red_sum[4][kWaves];
   __shared__ uint32_t red_arg[kWaves];
   const int64_t unit = blockIdx.x;
   const int64_t k = unit / nc;
@@ -229,18 +249,19 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
   float mt = zt[0], md = zd[0];
 #pragma unroll
   for (int i = 1; i < kEltsPerThread; ++i) {
-    mt = fmaxf(mt, zt[i]);
-    md = fmaxf(md, zd[i]);
+    mt = max_nan(mt, zt[i]);
+    md = max_nan(md, zd[i]);
   }
   const float Mt = block_max(mt, red[0]);
   const float Md = block_max(md, red[1]);
   if (greedy) wave_chunk_argmax<DT, VEC>(Mt, mt, [&](int i) { return zt[i]; }, chunk, red_arg);
   const float rt = Mt * c, rd = Md * c;
-  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  PairAcc s;
+  zero(s);
 #pragma unroll
   for (int i = 0; i < kEltsPerThread; i += 2) {
-    acc_pair(zt[i], zd[i], c, rt, rd, s[0], s[1], s[2], s[3]);
-    acc_pair(zt[i + 1], zd[i + 1], c, rt, rd, s[4], s[5], s[6], s[7]);
+    acc_pair(zt[i], zd[i], c, rt, rd, s, 0);
+    acc_pair(zt[i + 1], zd[i + 1], c, rt, rd, s, 1);
   }
   // a token outside [0, V) never matches (its sequence is flagged later)
   const int64_t local = int64_t(draft_tokens[w.pair]) - token_base - chunk * kChunk;
@@ -258,8 +279,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
       gathered[w.slot] = Gathered{a, b};
     }
   }
-  write_pair_chunk(rt, rd, s[0] + s[4], s[1] + s[5], s[2] + s[6], s[3] + s[7], red,
-                   out + int64_t(w.slot) * nc + chunk, Mt, red_arg,
+  write_pair_chunk(rt, rd, s, red_sum, out + int64_t(w.slot) * nc + chunk, Mt, red_arg,
                    greedy ? chunk_arg + int64_t(w.slot) * nc + chunk : nullptr);
 }
 

@@ -7,15 +7,20 @@ within 1e-6 probability mass of u' * Z).  Tie sequences are counted and checked
 only for validity (accepted drafts are a prefix of the drafted tokens, the rest
 is padding).
 
-Floating point: KLD and draft entropy within 1e-4 relative plus 1e-6 absolute.  The absolute
-floor comes from fp32 arithmetic: each log-probability difference entering KL
-is formed from fp32 values of magnitude up to ~10 (unit roundoff 6e-8), so a
-KL near 0 carries an absolute error of order 1e-7..1e-6.
+Floating point: KLD and draft entropy within 1e-4 relative plus 1e-7 absolute.
+The statistics pass sums each thread's 32 terms in fp32 and everything after
+that in fp64, so the row sums S_p, S_q and the KL accumulator A carry relative
+errors of a few fp32 roundings of the largest terms (~1e-7); KL = A/S_p -
+log S_p + log S_q turns relative errors e_p, e_q of the sums into an absolute
+error of about |e_q - e_p|, a few 1e-8 for these workloads (a CPU emulation
+of the kernel's summation order against the fp64 oracle gives at most 0.14
+of this tolerance on the b256 rows).  The 1e-7 floor covers KL values so
+small that 1e-4 of them is below that.
 """
 import numpy as np
 
-KLD_REL, KLD_ABS = 1e-4, 1e-6
-ENT_REL, ENT_ABS = 1e-4, 1e-6
+KLD_REL, KLD_ABS = 1e-4, 1e-7
+ENT_REL, ENT_ABS = 1e-4, 1e-7
 LSE_ABS = 2e-5
 
 
@@ -123,6 +128,8 @@ def compare_verify(got, ref, sl, cu_sl, label="", host=None):
         report["lse_max_abs_err"] = float(dl.max())
         assert dl.max() <= LSE_ABS, f"{label}: row lse off by {dl.max():.3g}"
     if pos_fine.any():
-        report["kld_max_rel_err"] = float((np.abs(kg[pos_fine] - kr[pos_fine]) /
-                                           np.maximum(np.abs(kr[pos_fine]), 1e-12)).max())
+        dk = np.abs(kg[pos_fine] - kr[pos_fine])
+        report["kld_max_rel_err"] = float((dk / np.maximum(np.abs(kr[pos_fine]), 1e-12)).max())
+        report["kld_max_abs_err"] = float(dk.max())
+        report["kld_err_over_tol"] = float((dk / (KLD_REL * np.abs(kr[pos_fine]) + KLD_ABS)).max())
     return report

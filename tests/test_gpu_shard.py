@@ -14,7 +14,7 @@ import torch
 
 import oracle
 import workloads as W
-from tests.parity import compare_verify
+from tests.parity import KLD_ABS, KLD_REL, compare_verify
 from tests.test_gpu_verify import announce, random_arrays, step_from_arrays
 
 pytestmark = pytest.mark.gpu
@@ -167,7 +167,7 @@ def test_sharded_equals_unsharded_on_kld(gpu_lib):
     split = run_sharded(dsde, step, dsde.slice_bounds(step.V, 8))
     assert np.array_equal(whole["seq_err"], split["seq_err"])
     d = np.abs(whole["kld"].astype(np.float64) - split["kld"].astype(np.float64))
-    assert (d <= 1e-4 * np.abs(whole["kld"]) + 1e-6).all(), d.max()
+    assert (d <= KLD_REL * np.abs(whole["kld"]) + KLD_ABS).all(), d.max()
 
 
 @pytest.mark.parametrize("name", ["b256", "greedy", "layout"])
