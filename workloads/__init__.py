@@ -25,6 +25,10 @@ are not available here):
   loop    B=1024, V=128256 bf16, 200 steps; per-sequence sigma follows a reflected
           random walk in [0.2, 4]; SL chosen each step by the controller; W=32,
           empty ring at the start; fresh logits every step.
+  spread  B=256, SL ~ U{1..8}, V=32000 bf16, close drafts (sigma ~ U[0.05, 0.6]) and a
+          per-sequence SL_max ~ U[4, 16] with next-step bound 16: small penalties
+          SF * WVIR, so the SL rule's decisions spread over many lengths instead of
+          collapsing onto SL_min.
 
 Zipf bias: row r gets b(v) = -s * ln(rank_r(v)) with rank_r(v) = ((a_r v + c_r) mod V) + 1
 and a_r coprime to V, a seeded bijection of the vocabulary, so exp(b) ~ rank^-s.
@@ -57,6 +61,9 @@ CONFIGS = {
     "batch8": dict(B=32, sl=("uniform", 1, 8), V=128256, dtype="bf16", sigma_z=4.0, zipf=1.05,
                    draft=("noise", 0.2, 4.0), temp=("alternate", 0.7, 1.0), W=32, sl_max=8.0, k_max=8,
                    prefill=True),
+    "spread": dict(B=256, sl=("uniform", 1, 8), V=32000, dtype="bf16", sigma_z=3.0, zipf=1.1,
+                   draft=("noise", 0.05, 0.6), temp=("all", 1.0), W=32, sl_max=("uniform", 4.0, 16.0),
+                   sl_hi=16, k_max=8, prefill=True),
     "loop": dict(B=1024, sl=("uniform", 2, 8), V=128256, dtype="bf16", sigma_z=4.0, zipf=1.05,
                  draft=("walk", 0.2, 4.0), temp=("all", 1.0), W=32, sl_max=8.0, k_max=8, prefill=False,
                  steps=200),
@@ -65,7 +72,7 @@ CONFIGS = {
 # stream tags: each random quantity has its own generator so that changing one
 # never shifts another
 _TAGS = {"sl": 1, "zipf": 2, "target": 3, "draft": 4, "tokens": 5, "uacc": 6, "ures": 7, "hist": 8,
-         "sigma": 9, "walk": 10}
+         "sigma": 9, "walk": 10, "slmax": 11}
 
 
 def _seed(seed, tag, step=0):
@@ -237,7 +244,7 @@ def make_step(cfg, seed=0, device="cpu", step=0, sl=None, sigma=None, V=None, B=
 
 
 def make_signal_state(cfg, seed=0, device="cpu", B=None):
-    """Ring of per-step mean KLD values.  Pre-filled rings hold W entries
+    """Ring of per-step mean KLD values and SL_max.  Pre-filled rings hold W entries
     h = kappa_b * exp(0.5 g) with kappa_b log-uniform in [0.02, 2]; for every
     fourth sequence the newest five entries are tripled (a recent burst of
     disagreement, which pushes WVIR above 1)."""
@@ -256,10 +263,14 @@ def make_signal_state(cfg, seed=0, device="cpu", B=None):
             for i in range(W):
                 hist[b, (head[b] - W + i) % W] = vals[b, i]
         count[:] = W
+    if isinstance(cfg["sl_max"], tuple):  # ("uniform", lo, hi): one SL_max per sequence
+        sl_max = _np_rng(seed, "slmax").uniform(cfg["sl_max"][1], cfg["sl_max"][2], B).astype(np.float32)
+    else:
+        sl_max = np.full(B, float(cfg["sl_max"]), np.float32)
     return SignalState(hist=torch.as_tensor(hist, device=device),
                        head=torch.as_tensor(head, device=device),
                        count=torch.as_tensor(count, device=device),
-                       sl_max=torch.full((B,), float(cfg["sl_max"]), device=device, dtype=torch.float32))
+                       sl_max=torch.as_tensor(sl_max, device=device))
 
 
 def host_arrays(step: Step):
