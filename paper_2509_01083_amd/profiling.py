@@ -28,13 +28,22 @@ CALIBRATION_KERNEL = "bitwise_not"
 CALIBRATION_BYTES = 1 << 30
 
 
-def kernel_source_hash():
-    """Hash of the sources the statistics kernel is built from."""
+STEP_SOURCES = ("stats.hip", "verify.hip", "signal.hip", "row_io.hpp", "common.hpp", "draw_device.hpp",
+                "signal_device.hpp", "lanes.hpp")
+
+
+def kernel_source_hash(files=("stats.hip", "row_io.hpp", "common.hpp")):
+    """Hash of the sources the statistics kernel (by default) is built from."""
     h = hashlib.sha256()
-    for f in ("stats.hip", "row_io.hpp", "common.hpp"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2509_01083_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
+
+
+def step_source_hash():
+    """Hash of the sources of every kernel of the verification step."""
+    return kernel_source_hash(STEP_SOURCES)
 
 
 def short_name(name):
@@ -85,6 +94,7 @@ def main():
     ap.add_argument("--write", help="WRITE_SIZE counter CSV")
     ap.add_argument("--workload", default="b256")
     ap.add_argument("--algorithmic-bytes", type=float)
+    ap.add_argument("--step-algorithmic-bytes", type=float, help="(2N + B_full) V e + I/O of the step")
     ap.add_argument("--json", help="traffic file to write (needs the counters)")
     ap.add_argument("--md", required=True)
     ap.add_argument("--command", action="append", default=[])
@@ -125,6 +135,15 @@ def main():
                "fetch_bytes_per_launch": f_k, "write_bytes_per_launch": w_k, "bytes_per_launch": f_k + w_k,
                "fetch_counter_scale": 1.0 / f_cal, "write_counter_scale": 1.0 / w_cal,
                "algorithmic_bytes": a.algorithmic_bytes}
+    # every kernel of the step (one launch each per step), for the step's traffic
+    step = {}
+    for k in sorted(set(fetch) & set(write)):
+        if k in (CALIBRATION_KERNEL, "stream_read_kernel"):
+            continue
+        step[k] = {"fetch_bytes": median(fetch[k]) * 1024 / f_cal, "write_bytes": median(write[k]) * 1024 / w_cal}
+    traffic["step_source_hash"] = step_source_hash()
+    traffic["step_kernels"] = step
+    traffic["step_bytes"] = sum(v["fetch_bytes"] + v["write_bytes"] for v in step.values())
     if a.json:
         with open(a.json, "w") as f:
             json.dump(traffic, f, indent=1)
@@ -155,6 +174,10 @@ def main():
     lines += ["", f"{KERNEL}: {traffic['bytes_per_launch'] / 1e6:.2f} MB per launch measured against "
               f"{a.algorithmic_bytes / 1e6:.2f} MB algorithmic "
               f"({traffic['bytes_per_launch'] / a.algorithmic_bytes:.4f}x).", ""]
+    if bench and a.step_algorithmic_bytes:
+        lines += [f"Step (every kernel above once): {traffic['step_bytes'] / 1e6:.2f} MB per step measured "
+                  f"against {a.step_algorithmic_bytes / 1e6:.2f} MB algorithmic "
+                  f"({traffic['step_bytes'] / a.step_algorithmic_bytes:.4f}x).", ""]
     with open(a.md, "w") as f:
         f.write("\n".join(lines))
 
