@@ -179,9 +179,11 @@ __device__ __forceinline__ float pick_bf16(const RawBf16 &r, int i) {
 // 1e-4 and below, and a thread's fp32 running sum near 1 (its largest
 // exponential is 1 at the chunk maximum) would round each later term to
 // about 6e-8 of it, leaving ~1e-7 of uncorrelated relative error in S_p and
-// S_q; summing the fp32 exponentials in fp64 leaves only their own rounding.
-// The KL and entropy accumulators enter the results through ratios to the
-// sums and stay fp32.
+// S_q.  The two exponentials of one bf16 word are added in fp32 (one
+// rounding) and the pair is added in fp64: half the conversions of per-term
+// fp64 sums, and as accurate for the KLD (groups of four were not, on
+// sharply peaked rows).  The KL and entropy accumulators enter the results
+// through ratios to the sums and stay fp32.
 struct PairAcc {
   double sp[2], sq[2];  // sum 2^at, sum 2^ad
   float a[2], h[2];     // sum 2^at (at - ad), sum 2^ad ad
@@ -191,26 +193,28 @@ __device__ __forceinline__ void zero(PairAcc &s) {
   s.a[0] = s.a[1] = s.h[0] = s.h[1] = 0.0f;
 }
 
-// Statistics of one logit pair with references rt, rd (log2 domain) into
-// accumulator set k: the two exponential sums, the KL accumulator
-// sum 2^at (at - ad), and the draft entropy accumulator sum 2^ad ad.
-__device__ __forceinline__ void acc_pair(float zt, float zd, float c, float rt, float rd, PairAcc &s, int k) {
-  const float at = fmaf(zt, c, -rt), ad = fmaf(zd, c, -rd);
-  const float et = fast_exp2(at), ed = fast_exp2(ad);
-  s.sp[k] += double(et);
-  s.sq[k] += double(ed);
-  s.a[k] = fmaf(et, at - ad, s.a[k]);
-  s.h[k] = fmaf(ed, ad, s.h[k]);
+// Statistics of two logit pairs (target zt0, zt1; draft zd0, zd1) with
+// references rt, rd (log2 domain) into accumulator set k: the two
+// exponential sums, the KL accumulator sum 2^at (at - ad), and the draft
+// entropy accumulator sum 2^ad ad.
+__device__ __forceinline__ void acc_two(float zt0, float zt1, float zd0, float zd1, float c, float rt, float rd,
+                                        PairAcc &s, int k) {
+  const float at0 = fmaf(zt0, c, -rt), ad0 = fmaf(zd0, c, -rd);
+  const float at1 = fmaf(zt1, c, -rt), ad1 = fmaf(zd1, c, -rd);
+  const float et0 = fast_exp2(at0), ed0 = fast_exp2(ad0);
+  const float et1 = fast_exp2(at1), ed1 = fast_exp2(ad1);
+  s.sp[k] += double(et0 + et1);
+  s.sq[k] += double(ed0 + ed1);
+  s.a[k] = fmaf(et1, at1 - ad1, fmaf(et0, at0 - ad0, s.a[k]));
+  s.h[k] = fmaf(ed1, ad1, fmaf(ed0, ad0, s.h[k]));
 }
-__device__ __forceinline__ void acc_word(uint32_t t, uint32_t d, float c, float rt, float rd, PairAcc &s) {
-  acc_pair(bf_lo(t), bf_lo(d), c, rt, rd, s, 0);
-  acc_pair(bf_hi(t), bf_hi(d), c, rt, rd, s, 1);
-}
+// The 8 bf16 pairs of one 16-byte load of each row, one word at a time,
+// words alternating between the two sets.
 __device__ __forceinline__ void acc_vec(uint4 t, uint4 d, float c, float rt, float rd, PairAcc &s) {
-  acc_word(t.x, d.x, c, rt, rd, s);
-  acc_word(t.y, d.y, c, rt, rd, s);
-  acc_word(t.z, d.z, c, rt, rd, s);
-  acc_word(t.w, d.w, c, rt, rd, s);
+  acc_two(bf_lo(t.x), bf_hi(t.x), bf_lo(d.x), bf_hi(d.x), c, rt, rd, s, 0);
+  acc_two(bf_lo(t.y), bf_hi(t.y), bf_lo(d.y), bf_hi(d.y), c, rt, rd, s, 1);
+  acc_two(bf_lo(t.z), bf_hi(t.z), bf_lo(d.z), bf_hi(d.z), c, rt, rd, s, 0);
+  acc_two(bf_lo(t.w), bf_hi(t.w), bf_lo(d.w), bf_hi(d.w), c, rt, rd, s, 1);
 }
 
 // Generic chunk of one row as 32 floats (fp32 rows, or rows without 16-byte alignment).

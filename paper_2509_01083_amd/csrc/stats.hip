@@ -259,9 +259,9 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
   PairAcc s;
   zero(s);
 #pragma unroll
-  for (int i = 0; i < kEltsPerThread; i += 2) {
-    acc_pair(zt[i], zd[i], c, rt, rd, s, 0);
-    acc_pair(zt[i + 1], zd[i + 1], c, rt, rd, s, 1);
+  for (int i = 0; i < kEltsPerThread; i += 4) {
+    acc_two(zt[i], zt[i + 1], zd[i], zd[i + 1], c, rt, rd, s, 0);
+    acc_two(zt[i + 2], zt[i + 3], zd[i + 2], zd[i + 3], c, rt, rd, s, 1);
   }
   // a token outside [0, V) never matches (its sequence is flagged later)
   const int64_t local = int64_t(draft_tokens[w.pair]) - token_base - chunk * kChunk;

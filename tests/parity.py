@@ -8,14 +8,19 @@ only for validity (accepted drafts are a prefix of the drafted tokens, the rest
 is padding).
 
 Floating point: KLD and draft entropy within 1e-4 relative plus 1e-7 absolute.
-The statistics pass sums each thread's 32 terms in fp32 and everything after
-that in fp64, so the row sums S_p, S_q and the KL accumulator A carry relative
-errors of a few fp32 roundings of the largest terms (~1e-7); KL = A/S_p -
-log S_p + log S_q turns relative errors e_p, e_q of the sums into an absolute
-error of about |e_q - e_p|, a few 1e-8 for these workloads (a CPU emulation
-of the kernel's summation order against the fp64 oracle gives at most 0.14
-of this tolerance on the b256 rows).  The 1e-7 floor covers KL values so
-small that 1e-4 of them is below that.
+The statistics pass computes each exponential in fp32, adds the two of one
+bf16 word in fp32 and everything after that in fp64.  KL = A/S_p - log S_p +
+log S_q then carries two kinds of error: relative errors e_p, e_q of the sums
+become an absolute KL error of about |e_q - e_p| (a few 1e-9 with these sums),
+and the fp32 rounding of the exponentials themselves, relative errors d_v
+and f_v of 2^(a_t) and 2^(a_d), shifts the result by about E_p[f - d] (the
+log-ratio the KL accumulator uses is that of the unrounded exponents), which
+reaches several 1e-8 when one token holds most of p.  A CPU emulation of the
+kernel's order of operations against the fp64 oracle gives at most 0.71 of
+this tolerance on 7,793 near-identical row pairs at V = 4096 and 0.56 on
+2,000 close-draft pairs at V = 32000 (fp32 running sums per thread reached
+1.2).  The 1e-7 floor covers KL values so small that 1e-4 of them is below
+that.
 """
 import numpy as np
 

@@ -240,7 +240,7 @@ def run_loop(dsde, cfg, steps, seed, label):
     st = W.make_signal_state(cfg, seed=seed, device="cuda")
     sl = W.sample_sl(cfg, seed)
     sigma = W.initial_sigma(cfg, seed)
-    total_ties, total_cmp, distinct = 0, 0, set()
+    total_ties, total_cmp, distinct, kld_ratio = 0, 0, set(), 0.0
     h_or, hd_or, c_or = st.hist.cpu().numpy().astype(np.float64), st.head.cpu().numpy(), st.count.cpu().numpy()
     for t in range(steps):
         step = W.make_step(cfg, seed=seed, device="cuda", step=t, sl=sl, sigma=sigma)
@@ -249,7 +249,8 @@ def run_loop(dsde, cfg, steps, seed, label):
         got = run_verify(dsde, step, row_lse=False)
         smax = st.sl_max.cpu().numpy().astype(np.float64)
         ref, sr, nr, spread = oracle_chain(host, h_or, hd_or, c_or, smax, cfg["k_max"])
-        compare_verify(got, ref, host["sl"], host["cu_sl"], f"{label} step {t}", host=host)
+        rep = compare_verify(got, ref, host["sl"], host["cu_sl"], f"{label} step {t}", host=host)
+        kld_ratio = max(kld_ratio, rep.get("kld_err_over_tol", 0.0))
         sg = gpu_signal(dsde, step.sl, step.cu_sl, torch.as_tensor(got["kld"], device="cuda"), st)
         compare_signal(sg, sr, f"{label} step {t} signal", spread)
         assert np.array_equal(st.head.cpu().numpy(), sr["head"]) and np.array_equal(st.count.cpu().numpy(),
@@ -266,7 +267,7 @@ def run_loop(dsde, cfg, steps, seed, label):
         sl = nr["sl_next"]
         sigma = W.walk_sigma(sigma, cfg, seed, t)
     print(f"[report] {label}: {steps} steps, SL ties {total_ties} of {total_cmp}, "
-          f"next lengths seen {sorted(distinct)}", flush=True)
+          f"next lengths seen {sorted(distinct)}, worst KLD error / tolerance {kld_ratio:.3f}", flush=True)
     assert total_ties <= MAX_SL_TIE_FRACTION * total_cmp
     if steps > cfg["W"]:
         assert (c_or == cfg["W"]).all()  # every ring filled and wrapped
