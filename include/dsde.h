@@ -222,6 +222,34 @@ int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t d
                   void *stream);
 
 /*
+ * dsde_step without a caller workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same kernels and bit-identical outputs, with the
+ * scratch space in a device array of DSDE_STATIC_SCRATCH_BYTES that the
+ * library holds, one copy per device, until the process ends.  The call
+ * allocates nothing; its first call on a device looks up that device's copy.
+ *
+ * Arguments as in dsde_step, less workspace and workspace_bytes.  Returns
+ * DSDE_WORKSPACE_TOO_SMALL when dsde_verify_workspace_bytes(B, N, V, k_max)
+ * exceeds DSDE_STATIC_SCRATCH_BYTES (nothing is enqueued), and
+ * DSDE_DEVICE_ERROR when the device copy cannot be found.  Every call on one
+ * device uses the same array: calls that may overlap on one device (several
+ * streams or threads) race and must be serialised by the caller.  No part of
+ * the array has to start at any value: every region a call reads is written
+ * earlier in that call.
+ */
+#define DSDE_STATIC_SCRATCH_BYTES (16u << 20)
+int32_t dsde_step_static(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
+                         int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl,
+                         const int32_t *draft_tokens, const float *temperature, const float *u_acc,
+                         const float *u_res, int32_t pad_id, int32_t *accepted, int32_t *tokens, float *kld,
+                         double *row_lse, float *draft_entropy, float *hist, int32_t *head, int32_t *count, int32_t W,
+                         int32_t n_short, int32_t n_long, float delta, float eps, float *mu_last, float *var_short,
+                         float *var_long, float *wvir, float *sf, const float *sl_max, float sl_min, int32_t sl_hi,
+                         const int32_t *budget, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
+                         void *stream);
+
+/*
  * SL_max calibration (Sec. 3.1.1, Eq. 1):
  *   SL_max = SL_A,max * (1 + mu_KLD,pre / (KLD_pre,max + eps))
  * over a few preliminary steps: SL_A,max the largest number of drafts accepted

@@ -18,8 +18,9 @@ OK, INVALID_ARG, WORKSPACE_TOO_SMALL, DEVICE_ERROR = 0, 1, 2, 3
 FP32, BF16 = 0, 1
 ERR_LAYOUT, ERR_TOKEN, ERR_LOGIT, ERR_TEMP, ERR_UNIFORM, ERR_SIGNAL, ERR_STATE = 1, 2, 4, 8, 16, 32, 64
 MAX_K = 63
+STATIC_SCRATCH_BYTES = 16 << 20  # DSDE_STATIC_SCRATCH_BYTES: the scratch array of dsde_step_static
 EXPORTS = ("dsde_abi_version", "dsde_status_string", "dsde_verify_workspace_bytes", "dsde_verify",
-           "dsde_step", "dsde_kld_signal", "dsde_next_sl", "dsde_calibration_update", "dsde_calibrate_sl_max",
+           "dsde_step", "dsde_step_static", "dsde_kld_signal", "dsde_next_sl", "dsde_calibration_update", "dsde_calibrate_sl_max",
            "dsde_set_profile_events", "dsde_stream_read", "dsde_shard_workspace_bytes", "dsde_shard_stats",
            "dsde_shard_accept", "dsde_shard_accept_step", "dsde_shard_draw_mass", "dsde_shard_draw_pick")
 # sizes of the records the vocabulary-shard calls exchange (dsde_shard_partial,
@@ -55,6 +56,10 @@ def load(path: str = LIB_PATH):
     lib.dsde_step.argtypes = [P, P, i32, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P, P,
                               P, P, P, i32, i32, i32, f32, f32, P, P, P, P, P,
                               P, f32, i32, P, P, P, P, P, P, sz, P]
+    lib.dsde_step_static.restype = i32
+    lib.dsde_step_static.argtypes = [P, P, i32, i64, i32, i64, i32, P, P, P, P, P, P, i32, P, P, P, P, P,
+                                     P, P, P, i32, i32, i32, f32, f32, P, P, P, P, P,
+                                     P, f32, i32, P, P, P, P, P, P]
     lib.dsde_kld_signal.restype = i32
     lib.dsde_kld_signal.argtypes = [i32, i64, P, P, P, P, P, P, i32, i32, i32, f32, f32, P, P, P, P, P, P, P]
     lib.dsde_next_sl.restype = i32
@@ -172,14 +177,9 @@ def _logits_dtype(target):
     raise DsdeError("logits must be bfloat16 or float32")
 
 
-def step(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, hist, head, count,
-         sl_max, n_short=10, n_long=30, delta=0.85, eps=1e-6, sl_min=2.0, sl_hi=None, pad_id=-1,
-         out=None, workspace=None, row_lse=None, draft_entropy=False, budget=None, stream=None):
-    """``dsde_step``: verify + signal update + SL rule in one call.  hist/head/count are
-    updated in place; returns a dict of every output (accepted, tokens, kld, mu_last,
-    var_short, var_long, wvir, sf, sl_hat, sl_cap, sl_next, seq_err, and draft_entropy
-    when asked for).  ``budget`` [B] int32: tokens each sequence may still emit."""
-    lib = load()
+def _step_args(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, hist, head, count,
+               sl_max, n_short, n_long, delta, eps, sl_min, sl_hi, pad_id, out, row_lse, draft_entropy, budget):
+    """Marshalled arguments of dsde_step up to seq_err (shared with dsde_step_static), and the outputs."""
     dt = _logits_dtype(target)
     V = int(target.shape[1])
     B = int(sl.shape[0])
@@ -201,10 +201,8 @@ def step(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_ma
     if draft_entropy and "draft_entropy" not in out:
         out["draft_entropy"] = torch.empty(max(N, 1), dtype=torch.float32, device=dev)[:N]
     ent = out.get("draft_entropy") if draft_entropy else None
-    if workspace is None:
-        workspace = new_workspace(B, N, V, k_max, device=dev)
     f32 = torch.float32
-    rc = lib.dsde_step(
+    args = [
         _ptr(target, name="target"), _ptr(draft, name="draft") if N > 0 else None, dt, V, B, N, k_max,
         _ptr(sl, torch.int32, B, "sl"), _ptr(cu_sl, torch.int32, B + 1, "cu_sl"),
         _ptr(draft_tokens, torch.int32, N, "draft_tokens") if N > 0 else None,
@@ -220,9 +218,40 @@ def step(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_ma
         _ptr(out["wvir"], f32, B), _ptr(out["sf"], f32, B), _ptr(sl_max, f32, B, "sl_max"), float(sl_min),
         int(sl_hi), _ptr(budget, torch.int32, B, "budget") if budget is not None else None,
         _ptr(out["sl_hat"], f32, B), _ptr(out["sl_cap"], f32, 1), _ptr(out["sl_next"], torch.int32, B),
-        _ptr(out["seq_err"], None, B), _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
-        _stream(stream))
+        _ptr(out["seq_err"], None, B)]
+    return args, out, (B, N, V)
+
+
+def step(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, hist, head, count,
+         sl_max, n_short=10, n_long=30, delta=0.85, eps=1e-6, sl_min=2.0, sl_hi=None, pad_id=-1,
+         out=None, workspace=None, row_lse=None, draft_entropy=False, budget=None, stream=None):
+    """``dsde_step``: verify + signal update + SL rule in one call.  hist/head/count are
+    updated in place; returns a dict of every output (accepted, tokens, kld, mu_last,
+    var_short, var_long, wvir, sf, sl_hat, sl_cap, sl_next, seq_err, and draft_entropy
+    when asked for).  ``budget`` [B] int32: tokens each sequence may still emit."""
+    lib = load()
+    args, out, (B, N, V) = _step_args(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max,
+                                      hist, head, count, sl_max, n_short, n_long, delta, eps, sl_min, sl_hi, pad_id,
+                                      out, row_lse, draft_entropy, budget)
+    if workspace is None:
+        workspace = new_workspace(B, N, V, k_max, device=target.device)
+    rc = lib.dsde_step(*args, _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(), _stream(stream))
     _check(rc)
+    return out
+
+
+def step_static(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, hist, head, count,
+                sl_max, n_short=10, n_long=30, delta=0.85, eps=1e-6, sl_min=2.0, sl_hi=None, pad_id=-1,
+                out=None, row_lse=None, draft_entropy=False, budget=None, stream=None):
+    """``dsde_step_static``: ``step`` without a workspace argument; the library's
+    per-device scratch array (STATIC_SCRATCH_BYTES) holds the scratch space, and
+    the call allocates no device memory when ``out`` is given.  Calls that may
+    overlap on one GPU share that array and must not run concurrently."""
+    lib = load()
+    args, out, _ = _step_args(target, draft, sl, cu_sl, draft_tokens, temperature, u_acc, u_res, k_max, hist, head,
+                              count, sl_max, n_short, n_long, delta, eps, sl_min, sl_hi, pad_id, out, row_lse,
+                              draft_entropy, budget)
+    _check(lib.dsde_step_static(*args, _stream(stream)))
     return out
 
 

@@ -2,6 +2,8 @@
 // workspace sizing and dispatch to the kernels.
 #include <math.h>
 
+#include <mutex>
+
 #include "common.hpp"
 #include "shard.hpp"
 
@@ -122,6 +124,94 @@ static int32_t signal_args(float *hist, int32_t *head, int32_t *count, int32_t W
   return DSDE_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Checks the arguments dsde_step and dsde_step_static share and packs them
+// (everything but the workspace).  The signal arguments live in `sg`, which
+// `a` points to.
+int32_t prepare_step(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
+                     int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
+                     const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
+                     int32_t *accepted, int32_t *tokens, float *kld, double *row_lse, float *draft_entropy,
+                     float *hist, int32_t *head, int32_t *count, int32_t W, int32_t n_short, int32_t n_long,
+                     float delta, float eps, float *mu_last, float *var_short, float *var_long, float *wvir,
+                     float *sf, const float *sl_max, float sl_min, int32_t sl_hi, const int32_t *budget,
+                     float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err, void *stream,
+                     dsde::VerifyArgs *a, dsde::SignalArgs *sg) {
+  if (dtype != DSDE_FP32 && dtype != DSDE_BF16) return DSDE_INVALID_ARG;
+  if (!verify_sizes_ok(B, N, V, k_max)) return DSDE_INVALID_ARG;
+  if (!target_logits || !sl || !cu_sl || !temperature || !u_res || !accepted || !tokens || !seq_err)
+    return DSDE_INVALID_ARG;
+  if (N > 0 && (!draft_logits || !draft_tokens || !u_acc || !kld)) return DSDE_INVALID_ARG;
+  const int32_t sst = signal_args(hist, head, count, W, n_short, n_long, delta, eps, mu_last, var_short, var_long,
+                                  wvir, sf, sl_max, sl_min, sl_hi, budget, sl_hat, sl_cap, sl_next, sg);
+  if (sst != DSDE_OK) return sst;
+  a->target = target_logits;
+  a->draft = draft_logits;
+  a->dtype = dtype;
+  a->V = V;
+  a->B = B;
+  a->N = N;
+  a->k_max = k_max;
+  a->sl = sl;
+  a->cu_sl = cu_sl;
+  a->draft_tokens = draft_tokens;
+  a->temperature = temperature;
+  a->u_acc = u_acc;
+  a->u_res = u_res;
+  a->pad_id = pad_id;
+  a->accepted = accepted;
+  a->tokens = tokens;
+  a->kld = kld;
+  a->seq_err = seq_err;
+  a->row_lse = row_lse;
+  a->draft_entropy = draft_entropy;
+  a->workspace = nullptr;
+  a->stream = static_cast<hipStream_t>(stream);
+  a->prof_start = g_prof_start;
+  a->prof_stop = g_prof_stop;
+  a->signal = sg;
+  return DSDE_OK;
+}
+
+// The workspace of dsde_step_static: one copy per device, kept until the
+// process ends.  Host code must never use the array's name as an address
+// (on the host it is a stand-in for the symbol); the device address of each
+// device's copy comes from hipGetSymbolAddress.
+__device__ __align__(256) static unsigned char scratch[DSDE_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the copy of `scratch` on the device `stream` belongs to
+// (the current device for the null stream), looked up on the first call
+// for that device with that device current.
+int32_t scratch_address(hipStream_t stream, void **out) {
+  int dev = -1, cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return DSDE_DEVICE_ERROR;
+  dev = cur;
+  if (stream && hipStreamGetDevice(stream, &dev) != hipSuccess) return DSDE_DEVICE_ERROR;
+  if (dev < 0 || dev >= kMaxDevices) return DSDE_DEVICE_ERROR;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    if (dev != cur && hipSetDevice(dev) != hipSuccess) return DSDE_DEVICE_ERROR;
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur && hipSetDevice(cur) != hipSuccess) return DSDE_DEVICE_ERROR;
+    if (e != hipSuccess || !p) return DSDE_DEVICE_ERROR;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DSDE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
                   int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl, const int32_t *draft_tokens,
                   const float *temperature, const float *u_acc, const float *u_res, int32_t pad_id,
@@ -131,44 +221,49 @@ int32_t dsde_step(const void *target_logits, const void *draft_logits, int32_t d
                   const float *sl_max, float sl_min, int32_t sl_hi, const int32_t *budget, float *sl_hat,
                   float *sl_cap, int32_t *sl_next, uint32_t *seq_err, void *workspace, size_t workspace_bytes,
                   void *stream) {
-  if (dtype != DSDE_FP32 && dtype != DSDE_BF16) return DSDE_INVALID_ARG;
-  if (!verify_sizes_ok(B, N, V, k_max)) return DSDE_INVALID_ARG;
-  if (!target_logits || !sl || !cu_sl || !temperature || !u_res || !accepted || !tokens || !seq_err ||
-      !workspace)
-    return DSDE_INVALID_ARG;
-  if (N > 0 && (!draft_logits || !draft_tokens || !u_acc || !kld)) return DSDE_INVALID_ARG;
+  dsde::VerifyArgs a;
   dsde::SignalArgs sg;
-  const int32_t sst = signal_args(hist, head, count, W, n_short, n_long, delta, eps, mu_last, var_short, var_long,
-                                  wvir, sf, sl_max, sl_min, sl_hi, budget, sl_hat, sl_cap, sl_next, &sg);
-  if (sst != DSDE_OK) return sst;
+  const int32_t st = prepare_step(target_logits, draft_logits, dtype, V, B, N, k_max, sl, cu_sl, draft_tokens,
+                                  temperature, u_acc, u_res, pad_id, accepted, tokens, kld, row_lse, draft_entropy,
+                                  hist, head, count, W, n_short, n_long, delta, eps, mu_last, var_short, var_long,
+                                  wvir, sf, sl_max, sl_min, sl_hi, budget, sl_hat, sl_cap, sl_next, seq_err, stream,
+                                  &a, &sg);
+  if (st != DSDE_OK) return st;
+  if (!workspace) return DSDE_INVALID_ARG;
   if (workspace_bytes < dsde::workspace_layout(B, N, V, k_max).total) return DSDE_WORKSPACE_TOO_SMALL;
   if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return DSDE_INVALID_ARG;
-  dsde::VerifyArgs a;
-  a.target = target_logits;
-  a.draft = draft_logits;
-  a.dtype = dtype;
-  a.V = V;
-  a.B = B;
-  a.N = N;
-  a.k_max = k_max;
-  a.sl = sl;
-  a.cu_sl = cu_sl;
-  a.draft_tokens = draft_tokens;
-  a.temperature = temperature;
-  a.u_acc = u_acc;
-  a.u_res = u_res;
-  a.pad_id = pad_id;
-  a.accepted = accepted;
-  a.tokens = tokens;
-  a.kld = kld;
-  a.seq_err = seq_err;
-  a.row_lse = row_lse;
-  a.draft_entropy = draft_entropy;
   a.workspace = workspace;
-  a.stream = static_cast<hipStream_t>(stream);
-  a.prof_start = g_prof_start;
-  a.prof_stop = g_prof_stop;
-  a.signal = &sg;
+  return dsde::launch_verify(a);
+}
+
+int32_t dsde_step_static(const void *target_logits, const void *draft_logits, int32_t dtype, int64_t V, int32_t B,
+                         int64_t N, int32_t k_max, const int32_t *sl, const int32_t *cu_sl,
+                         const int32_t *draft_tokens, const float *temperature, const float *u_acc,
+                         const float *u_res, int32_t pad_id, int32_t *accepted, int32_t *tokens, float *kld,
+                         double *row_lse, float *draft_entropy, float *hist, int32_t *head, int32_t *count, int32_t W,
+                         int32_t n_short, int32_t n_long, float delta, float eps, float *mu_last, float *var_short,
+                         float *var_long, float *wvir, float *sf, const float *sl_max, float sl_min, int32_t sl_hi,
+                         const int32_t *budget, float *sl_hat, float *sl_cap, int32_t *sl_next, uint32_t *seq_err,
+                         void *stream) {
+  dsde::VerifyArgs a;
+  dsde::SignalArgs sg;
+  const int32_t st = prepare_step(target_logits, draft_logits, dtype, V, B, N, k_max, sl, cu_sl, draft_tokens,
+                                  temperature, u_acc, u_res, pad_id, accepted, tokens, kld, row_lse, draft_entropy,
+                                  hist, head, count, W, n_short, n_long, delta, eps, mu_last, var_short, var_long,
+                                  wvir, sf, sl_max, sl_min, sl_hi, budget, sl_hat, sl_cap, sl_next, seq_err, stream,
+                                  &a, &sg);
+  if (st != DSDE_OK) return st;
+  // every region of the workspace a call reads is written earlier in the same
+  // call, so the array needs no clearing between calls
+  if (dsde::workspace_layout(B, N, V, k_max).total > size_t(DSDE_STATIC_SCRATCH_BYTES))
+    return DSDE_WORKSPACE_TOO_SMALL;
+  void *ws = nullptr;
+  const int32_t sa = scratch_address(a.stream, &ws);
+  if (sa != DSDE_OK) {
+    (void)hipGetLastError();
+    return sa;
+  }
+  a.workspace = ws;
   return dsde::launch_verify(a);
 }
 

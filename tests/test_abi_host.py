@@ -250,3 +250,42 @@ def test_slice_bounds_tile_the_vocabulary():
         b = dsde.slice_bounds(V, G)
         assert b[0][0] == 0 and b[-1][1] == V and len(b) <= G
         assert all(b[i][1] == b[i + 1][0] and b[i][0] < b[i][1] for i in range(len(b) - 1))
+
+
+def _step_static_args(**over):
+    a = dict(target=FAKE, draft=FAKE, dtype=1, V=1000, B=4, N=8, k_max=4, sl=FAKE, cu_sl=FAKE, toks=FAKE,
+             temp=FAKE, u_acc=FAKE, u_res=FAKE, pad=-1, acc=FAKE, tokens=FAKE, kld=FAKE, lse=None, ent=None,
+             hist=FAKE, head=FAKE, count=FAKE, W=32, n_short=10, n_long=30, delta=0.85, eps=1e-6,
+             mu_last=FAKE, var_short=FAKE, var_long=FAKE, wvir=FAKE, sf=FAKE, sl_max=FAKE, sl_min=2.0, sl_hi=8,
+             budget=None, sl_hat=FAKE, sl_cap=FAKE, sl_next=FAKE, err=FAKE, stream=None)
+    a.update(over)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("over", [
+    dict(dtype=2), dict(B=0), dict(V=0), dict(k_max=64), dict(target=None), dict(draft=None), dict(acc=None),
+    dict(err=None), dict(W=0), dict(n_short=31), dict(eps=0.0), dict(hist=None), dict(sl_max=None),
+    dict(sl_min=9.0), dict(sl_next=None),
+])
+def test_step_static_rejects_invalid_arguments(lib, over):
+    """The allocation-free fused step checks dsde_step's arguments (less the
+    workspace) before any HIP call."""
+    assert lib.dsde_step_static(*_step_static_args(**over)) == 1
+
+
+def test_step_static_rejects_shapes_beyond_its_scratch(lib):
+    import paper_2509_01083_amd as dsde
+    # B = 1024 sequences with k_max = 63 at V = 128256 need ~56 MB of scratch
+    B, k_max, V = 1024, 63, 128256
+    N = B * k_max
+    assert lib.dsde_verify_workspace_bytes(B, N, V, k_max) > dsde.STATIC_SCRATCH_BYTES
+    assert lib.dsde_step_static(*_step_static_args(B=B, N=N, V=V, k_max=k_max, sl_hi=63)) == 2
+    # every configuration of the benchmark fits
+    for B, N, V, k in ((256, 2048, 128256, 8), (512, 8192, 152064, 16), (1024, 8192, 128256, 8)):
+        assert 0 < lib.dsde_verify_workspace_bytes(B, N, V, k) <= dsde.STATIC_SCRATCH_BYTES
+
+
+def test_static_scratch_size_matches_header():
+    import paper_2509_01083_amd as dsde
+    m = re.search(r"#define DSDE_STATIC_SCRATCH_BYTES \((\d+)u << (\d+)\)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == dsde.STATIC_SCRATCH_BYTES
