@@ -82,6 +82,28 @@
 #define ORC_TIE_BAND 1e-6
 
 /* ------------------------------------------------------------------ */
+/* compensated sums                                                    */
+/* ------------------------------------------------------------------ */
+
+/* Neumaier's compensated summation: the running sum s, and in c the
+ * low-order part every addition rounded away (taken from whichever operand
+ * is smaller in magnitude); the sum is s + c. */
+typedef struct {
+  double s, c;
+} csum;
+
+static void csum_add(csum *a, double x) {
+  double t = a->s + x;
+  if (fabs(a->s) >= fabs(x))
+    a->c += (a->s - t) + x;
+  else
+    a->c += (x - t) + a->s;
+  a->s = t;
+}
+
+static double csum_value(const csum *a) { return a->s + a->c; }
+
+/* ------------------------------------------------------------------ */
 /* logits                                                              */
 /* ------------------------------------------------------------------ */
 
@@ -109,9 +131,9 @@ static double row_lse(const void *base, int dtype, int64_t V, int64_t row, doubl
     double s = logit(base, dtype, V, row, v) / T;
     if (s > m) m = s;
   }
-  double S = 0.0;
-  for (int64_t v = 0; v < V; ++v) S += exp(logit(base, dtype, V, row, v) / T - m);
-  return m + log(S);
+  csum S = {0.0, 0.0};
+  for (int64_t v = 0; v < V; ++v) csum_add(&S, exp(logit(base, dtype, V, row, v) / T - m));
+  return m + log(csum_value(&S));
 }
 
 /* The smallest token id holding the row's largest logit. */
@@ -201,23 +223,24 @@ static void verify_sequence(const verify_job *J, int32_t b) {
     lse_p[j] = row_lse(J->target, J->dtype, V, tr, T);
     lse_q[j] = row_lse(J->draft, J->dtype, V, dr, T);
     /* KL(p || q) = sum_v p_v (log p_v - log q_v); terms with p_v == 0 vanish */
-    double kl = 0.0;
+    csum kls = {0.0, 0.0};
     for (int64_t v = 0; v < V; ++v) {
       double lp = logit(J->target, J->dtype, V, tr, v) / T - lse_p[j];
       double lq = logit(J->draft, J->dtype, V, dr, v) / T - lse_q[j];
       double p = exp(lp);
-      if (p > 0.0) kl += p * (lp - lq);
+      if (p > 0.0) csum_add(&kls, p * (lp - lq));
     }
+    const double kl = csum_value(&kls);
     J->kld[first + j] = kl > 0.0 ? kl : 0.0;
     if (J->entropy) {
       /* H(q) = -sum_v q_v log q_v of the same tempered draft distribution */
-      double h = 0.0;
+      csum h = {0.0, 0.0};
       for (int64_t v = 0; v < V; ++v) {
         double lq = logit(J->draft, J->dtype, V, dr, v) / T - lse_q[j];
         double q = exp(lq);
-        if (q > 0.0) h -= q * lq;
+        if (q > 0.0) csum_add(&h, -q * lq);
       }
-      J->entropy[first + j] = h;
+      J->entropy[first + j] = csum_value(&h);
     }
     if (J->lse) {
       J->lse[2 * (first + j)] = lse_p[j];
@@ -282,7 +305,7 @@ static void verify_sequence(const verify_job *J, int32_t b) {
     lp_row = row_lse(J->target, J->dtype, V, tr, T);
   }
   double *w = (double *)malloc(sizeof(double) * (size_t)V);
-  double Z = 0.0;
+  csum Zs = {0.0, 0.0};
   for (int64_t v = 0; v < V; ++v) {
     double p = exp(logit(J->target, J->dtype, V, tr, v) / T - lp_row);
     if (dr >= 0) {
@@ -291,20 +314,24 @@ static void verify_sequence(const verify_job *J, int32_t b) {
     } else {
       w[v] = p;
     }
-    Z += w[v];
+    csum_add(&Zs, w[v]);
   }
-  if (Z == 0.0) { /* no residual mass left: draw from p of the same target row */
+  if (csum_value(&Zs) == 0.0) { /* no residual mass left: draw from p of the same target row */
     for (int64_t v = 0; v < V; ++v) {
       w[v] = exp(logit(J->target, J->dtype, V, tr, v) / T - lp_row);
-      Z += w[v];
+      csum_add(&Zs, w[v]);
     }
   }
+  const double Z = csum_value(&Zs);
   const double target_mass = (double)J->u_res[b] * Z;
+  /* the cumulative weight C(v) in ascending token id, compensated like Z */
   int64_t y = -1;
+  csum Cs = {0.0, 0.0};
   double C = 0.0, C_prev = 0.0;
   for (int64_t v = 0; v < V; ++v) {
     C_prev = C;
-    C += w[v];
+    csum_add(&Cs, w[v]);
+    C = csum_value(&Cs);
     if (C > target_mass) {
       y = v;
       break;

@@ -99,6 +99,7 @@ def main():
     ap.add_argument("--md", required=True)
     ap.add_argument("--command", action="append", default=[])
     ap.add_argument("--bench-log", help="output of bench.py run without the profiler (its last line is the JSON)")
+    ap.add_argument("--title", help="heading of the summary (default: the statistics kernel and the workload)")
     a = ap.parse_args()
     bench = None
     if a.bench_log:
@@ -106,7 +107,8 @@ def main():
             bench = json.loads(f.read().strip().splitlines()[-1])
     cfg = bench["config"] if bench else {}
     shape = ", ".join(f"{k}={cfg[k]}" for k in ("B", "N", "V") if k in cfg)
-    lines = [f"# {KERNEL}, workload {a.workload}" + (f" ({shape}, bf16)" if shape else ""), "",
+    title = a.title or f"{KERNEL}, workload {a.workload}"
+    lines = [f"# {title}" + (f" ({shape}, bf16)" if shape else ""), "",
              "Commands (from the repository root):", ""]
     lines += [f"    {c}" for c in a.command]
     lines += ["", "## Kernel durations (rocprofv3 --kernel-trace --stats)", "",

@@ -15,9 +15,9 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "dsde_oracle.c")
 
 MUTANTS = {
-    "kl_direction": ("if (p > 0.0) kl += p * (lp - lq);", "if (p > 0.0) kl += p * (lq - lp);"),
-    "no_temperature_in_lse": ("S += exp(logit(base, dtype, V, row, v) / T - m);",
-                              "S += exp(logit(base, dtype, V, row, v) - m);"),
+    "kl_direction": ("if (p > 0.0) csum_add(&kls, p * (lp - lq));", "if (p > 0.0) csum_add(&kls, p * (lq - lp));"),
+    "no_temperature_in_lse": ("csum_add(&S, exp(logit(base, dtype, V, row, v) / T - m));",
+                              "csum_add(&S, exp(logit(base, dtype, V, row, v) - m));"),
     "residual_sign": ("w[v] = p - q > 0.0 ? p - q : 0.0;", "w[v] = q - p > 0.0 ? q - p : 0.0;"),
     "target_row_index": ("const int64_t trow0 = first + b;", "const int64_t trow0 = first;"),
     "bonus_row_index": ("tr = trow0 + SL;", "tr = trow0 + SL - 1;"),
@@ -28,6 +28,7 @@ MUTANTS = {
     "bessel_variance": ("*var = sv / sa;", "*var = sv / (sa - 1.0);"),
     "weights_reversed": ("double alpha = pow(delta, (double)(i - 1));\n    sa += alpha;",
                          "double alpha = pow(delta, (double)(n - i));\n    sa += alpha;"),
+    "cdf_weights_rescaled": ("    csum_add(&Cs, w[v]);\n    C = csum_value(&Cs);", "    C += w[v] * (1.0 + 1e-9);"),
     "wvir_guard_always_added": ("*wvir = *var_s / (*var_l > 0.0 ? *var_l : eps);",
                                 "*wvir = *var_s / (*var_l + eps);"),
     "window_not_shifted": ("sad += alpha * (newest_first[i - 1] - h1);", "sad += alpha * newest_first[i - 1];"),
@@ -41,7 +42,7 @@ MUTANTS = {
     "greedy_tie_takes_last": ("    if (z > m) {\n      m = z;\n      best = v;", "    if (z >= m) {\n      m = z;\n      best = v;"),
     "greedy_emits_next_row": ("tok[a] = (int32_t)row_argmax(J->target, J->dtype, V, trow0 + a);",
                               "tok[a] = (int32_t)row_argmax(J->target, J->dtype, V, trow0 + a + (a < SL));"),
-    "entropy_sign": ("if (q > 0.0) h -= q * lq;", "if (q > 0.0) h += q * lq;"),
+    "entropy_sign": ("if (q > 0.0) csum_add(&h, -q * lq);", "if (q > 0.0) csum_add(&h, q * lq);"),
     "budget_off_by_one": ("int32_t room = budget[b] - 1 > 0 ? budget[b] - 1 : 0;",
                           "int32_t room = budget[b] > 0 ? budget[b] : 0;"),
     "greedy_kld_at_zero_scale": ("const double T = greedy ? 1.0 : (double)J->temperature[b];",
