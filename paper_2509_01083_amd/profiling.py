@@ -100,6 +100,10 @@ def main():
     ap.add_argument("--command", action="append", default=[])
     ap.add_argument("--bench-log", help="output of bench.py run without the profiler (its last line is the JSON)")
     ap.add_argument("--title", help="heading of the summary (default: the statistics kernel and the workload)")
+    ap.add_argument("--counter", action="append", default=[],
+                    help="NAME=CSV: a --pmc run of one counter, tabulated per kernel (mean over dispatches)")
+    ap.add_argument("--elements", type=float,
+                    help="element pairs one launch of the statistics kernel processes (for VALU per element)")
     a = ap.parse_args()
     bench = None
     if a.bench_log:
@@ -115,6 +119,23 @@ def main():
               "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
     for k, n, avg, lo, hi in trace_stats(a.trace):
         lines.append(f"| {k} | {n} | {avg:.2f} | {lo:.2f} | {hi:.2f} |")
+    if a.counter:
+        names = [c.split("=", 1)[0] for c in a.counter]
+        vals = {n: counter_values(c.split("=", 1)[1], n) for n, c in zip(names, a.counter)}
+        kernels = sorted(set().union(*(set(v) for v in vals.values())) - {CALIBRATION_KERNEL})
+        lines += ["", "## Counters (rocprofv3 --pmc, one counter per run; mean over each kernel's dispatches)", "",
+                  "| kernel | " + " | ".join(names) + " |", "|---|" + "---|" * len(names)]
+        for k in kernels:
+            cells = []
+            for n in names:
+                v = vals[n].get(k)
+                cells.append(f"{sum(v) / len(v):,.1f}" if v else "")
+            lines.append(f"| {k} | " + " | ".join(cells) + " |")
+        if a.elements and "SQ_INSTS_VALU" in vals and KERNEL in vals["SQ_INSTS_VALU"]:
+            v = vals["SQ_INSTS_VALU"][KERNEL]
+            per = sum(v) / len(v) / a.elements * 64
+            lines += ["", f"{KERNEL}: {a.elements:,.0f} element pairs per launch, {per:.1f} VALU wave "
+                      "instructions per 64 element pairs."]
     if not (a.fetch and a.write):
         if bench and "loop" in bench:
             lp = bench["loop"]
