@@ -63,10 +63,11 @@ def parse():
 
 def stats_kernel_name(esz, V):
     """The statistics kernel the library dispatches for this row layout (the
-    bench's tensors are 16-byte aligned): the bf16 vector kernel, else the
-    generic one instantiated for the dtype and vector width."""
+    bench's tensors are 16-byte aligned): the bf16 vector kernel in its form
+    without the draft-entropy accumulator (the step asks for no entropy), else
+    the generic one instantiated for the dtype and vector width."""
     if esz == 2:
-        return "stats_kernel_bf16" if V % 8 == 0 else "stats_kernel_generic<bf16, scalar>"
+        return "stats_kernel_bf16<false>" if V % 8 == 0 else "stats_kernel_generic<bf16, scalar>"
     return "stats_kernel_generic<fp32, vec4>" if V % 4 == 0 else "stats_kernel_generic<fp32, scalar>"
 
 

@@ -130,7 +130,10 @@ struct VerifyArgs {
 
 int launch_verify(const VerifyArgs &a);
 // The set-up and statistics kernels of one verification step (stats.hip).
-void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gathered *gath, ChunkArg *chunk_arg);
+// With `entropy` false the bf16 statistics kernel leaves the draft entropy
+// accumulator (PairChunk::h) at zero.
+void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gathered *gath, ChunkArg *chunk_arg,
+                       bool entropy);
 // Rows are 16-byte aligned and V a multiple of the vector width.
 bool rows_vectorizable(const VerifyArgs &a);
 int launch_kld_signal(int32_t B, int64_t N, const int32_t *sl, const int32_t *cu_sl, const float *kld,

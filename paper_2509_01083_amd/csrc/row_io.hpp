@@ -156,7 +156,8 @@ __device__ __forceinline__ RawBf16 load_raw_bf16(const void *row, int64_t V, int
 // Larger of two floats, NaN if either is NaN (the IEEE 754-2019 maximum:
 // v_maximum3_f32 on gfx950).  fmaxf would first quiet every loaded value
 // (one v_max_f32 x, x, x per logit in IEEE mode).  A NaN logit makes its
-// chunk maximum NaN, and with it every sum of the chunk, so the row is
+// thread's maximum NaN (the cross-lane fmaxf steps of block_max may drop
+// it), and its exponential makes every sum of the chunk NaN, so the row is
 // flagged as with fmaxf.
 __device__ __forceinline__ float max_nan(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 __device__ __forceinline__ float max2(uint32_t w) { return max_nan(bf_lo(w), bf_hi(w)); }
@@ -195,8 +196,9 @@ __device__ __forceinline__ void zero(PairAcc &s) {
 
 // Statistics of two logit pairs (target zt0, zt1; draft zd0, zd1) with
 // references rt, rd (log2 domain) into accumulator set k: the two
-// exponential sums, the KL accumulator sum 2^at (at - ad), and the draft
-// entropy accumulator sum 2^ad ad.
+// exponential sums, the KL accumulator sum 2^at (at - ad), and, with ENT, the
+// draft entropy accumulator sum 2^ad ad (left at zero without it).
+template <bool ENT>
 __device__ __forceinline__ void acc_two(float zt0, float zt1, float zd0, float zd1, float c, float rt, float rd,
                                         PairAcc &s, int k) {
   const float at0 = fmaf(zt0, c, -rt), ad0 = fmaf(zd0, c, -rd);
@@ -206,15 +208,16 @@ __device__ __forceinline__ void acc_two(float zt0, float zt1, float zd0, float z
   s.sp[k] += double(et0 + et1);
   s.sq[k] += double(ed0 + ed1);
   s.a[k] = fmaf(et1, at1 - ad1, fmaf(et0, at0 - ad0, s.a[k]));
-  s.h[k] = fmaf(ed1, ad1, fmaf(ed0, ad0, s.h[k]));
+  if constexpr (ENT) s.h[k] = fmaf(ed1, ad1, fmaf(ed0, ad0, s.h[k]));
 }
 // The 8 bf16 pairs of one 16-byte load of each row, one word at a time,
 // words alternating between the two sets.
+template <bool ENT>
 __device__ __forceinline__ void acc_vec(uint4 t, uint4 d, float c, float rt, float rd, PairAcc &s) {
-  acc_two(bf_lo(t.x), bf_hi(t.x), bf_lo(d.x), bf_hi(d.x), c, rt, rd, s, 0);
-  acc_two(bf_lo(t.y), bf_hi(t.y), bf_lo(d.y), bf_hi(d.y), c, rt, rd, s, 1);
-  acc_two(bf_lo(t.z), bf_hi(t.z), bf_lo(d.z), bf_hi(d.z), c, rt, rd, s, 0);
-  acc_two(bf_lo(t.w), bf_hi(t.w), bf_lo(d.w), bf_hi(d.w), c, rt, rd, s, 1);
+  acc_two<ENT>(bf_lo(t.x), bf_hi(t.x), bf_lo(d.x), bf_hi(d.x), c, rt, rd, s, 0);
+  acc_two<ENT>(bf_lo(t.y), bf_hi(t.y), bf_lo(d.y), bf_hi(d.y), c, rt, rd, s, 1);
+  acc_two<ENT>(bf_lo(t.z), bf_hi(t.z), bf_lo(d.z), bf_hi(d.z), c, rt, rd, s, 0);
+  acc_two<ENT>(bf_lo(t.w), bf_hi(t.w), bf_lo(d.w), bf_hi(d.w), c, rt, rd, s, 1);
 }
 
 // Generic chunk of one row as 32 floats (fp32 rows, or rows without 16-byte alignment).

@@ -572,7 +572,9 @@ int launch_shard_stats(const ShardRows &r, int64_t V, const int32_t *sl, const i
   PairChunk *pc = (PairChunk *)(ws + L.stats.pair_chunk);
   Gathered *gath = (Gathered *)(ws + L.stats.gathered);
   ChunkArg *cargs = (ChunkArg *)(ws + L.stats.chunk_arg);
-  launch_stats_pass(a, work, pc, gath, cargs);
+  // the shard partial always carries the entropy accumulator: whether a
+  // caller wants the entropy is known only when the partials are combined
+  launch_stats_pass(a, work, pc, gath, cargs, true);
   if (r.N > 0) {
     const int32_t nc = int32_t(num_chunks(r.V_shard));
     const dim3 grid(unsigned(r.B)), block(kShardThreads);

@@ -159,7 +159,12 @@ __device__ __forceinline__ void write_pair_chunk(float rt, float rd, const PairA
   }
 }
 
-// bf16 rows with 16-byte alignment: the hot kernel.
+// bf16 rows with 16-byte alignment: the hot kernel.  ENT: accumulate the
+// draft entropy, only for callers that ask for it (one FMA of about twenty
+// VALU instructions per logit pair).  Two kernels rather than a branch in
+// one: with both forms in one body the compiler hoists their common
+// arithmetic above the branch and nearly doubles the register footprint.
+template <bool ENT>
 __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__restrict__ target,
                                                              const void *__restrict__ draft, int64_t V, int32_t nc,
                                                              const WorkItem *__restrict__ work,
@@ -192,10 +197,10 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_bf16(const void *__rest
   const float rt = Mt * c, rd = Md * c;
   PairAcc s;
   zero(s);
-  acc_vec(rt_.v0, rd_.v0, c, rt, rd, s);
-  acc_vec(rt_.v1, rd_.v1, c, rt, rd, s);
-  acc_vec(rt_.v2, rd_.v2, c, rt, rd, s);
-  acc_vec(rt_.v3, rd_.v3, c, rt, rd, s);
+  acc_vec<ENT>(rt_.v0, rd_.v0, c, rt, rd, s);
+  acc_vec<ENT>(rt_.v1, rd_.v1, c, rt, rd, s);
+  acc_vec<ENT>(rt_.v2, rd_.v2, c, rt, rd, s);
+  acc_vec<ENT>(rt_.v3, rd_.v3, c, rt, rd, s);
 
   // the logits at the drafted token, from registers
   // a token outside [0, V) never matches (its sequence is flagged later)
@@ -260,8 +265,8 @@ __global__ __launch_bounds__(kThreads) void stats_kernel_generic(const void *__r
   zero(s);
 #pragma unroll
   for (int i = 0; i < kEltsPerThread; i += 4) {
-    acc_two(zt[i], zt[i + 1], zd[i], zd[i + 1], c, rt, rd, s, 0);
-    acc_two(zt[i + 2], zt[i + 3], zd[i + 2], zd[i + 3], c, rt, rd, s, 1);
+    acc_two<true>(zt[i], zt[i + 1], zd[i], zd[i + 1], c, rt, rd, s, 0);
+    acc_two<true>(zt[i + 2], zt[i + 3], zd[i + 2], zd[i + 3], c, rt, rd, s, 1);
   }
   // a token outside [0, V) never matches (its sequence is flagged later)
   const int64_t local = int64_t(draft_tokens[w.pair]) - token_base - chunk * kChunk;
@@ -305,7 +310,8 @@ bool rows_vectorizable(const VerifyArgs &a) {
          (a.dtype == DSDE_BF16 ? a.V % 8 == 0 : a.V % 4 == 0);
 }
 
-void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gathered *gath, ChunkArg *chunk_arg) {
+void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gathered *gath, ChunkArg *chunk_arg,
+                       bool entropy) {
   const int32_t nc = int32_t(num_chunks(a.V));
   const bool prof = a.prof_start && a.prof_stop && a.N > 0;
   launch_timed(setup_kernel, dim3(1), dim3(1024), a.stream, prof ? a.prof_start : nullptr, a.B, a.N, a.k_max,
@@ -319,8 +325,11 @@ void launch_stats_pass(const VerifyArgs &a, WorkItem *work, PairChunk *part, Gat
   const int32_t *tokens = a.draft_tokens;
   const int64_t base = a.token_base;
   const WorkItem *w = work;
-  if (a.dtype == DSDE_BF16 && vec)
-    launch_timed(stats_kernel_bf16, grid, block, a.stream, done, T, D, V, nc, w, tokens, base, part, gath,
+  if (a.dtype == DSDE_BF16 && vec && entropy)
+    launch_timed(stats_kernel_bf16<true>, grid, block, a.stream, done, T, D, V, nc, w, tokens, base, part, gath,
+                 chunk_arg);
+  else if (a.dtype == DSDE_BF16 && vec)
+    launch_timed(stats_kernel_bf16<false>, grid, block, a.stream, done, T, D, V, nc, w, tokens, base, part, gath,
                  chunk_arg);
   else if (a.dtype == DSDE_BF16)
     launch_timed(stats_kernel_generic<DSDE_BF16, false>, grid, block, a.stream, done, T, D, V, nc, w, tokens, base,

@@ -564,7 +564,7 @@ int launch_verify(const VerifyArgs &a) {
   Gathered *gath = (Gathered *)(ws + L.gathered);
   (void)hipGetLastError();
   ChunkArg *cargs = (ChunkArg *)(ws + L.chunk_arg);
-  launch_stats_pass(a, work, part, gath, cargs);
+  launch_stats_pass(a, work, part, gath, cargs, a.draft_entropy != nullptr);
   const bool vec = rows_vectorizable(a);
   StepParams P;
   P.target = a.target;

@@ -49,8 +49,6 @@ def step_source_hash():
 def short_name(name):
     m = re.search(r"dsde::\(anonymous namespace\)::(\w+)(<[^>(]*>)?", name)
     if m:
-        if m.group(1) == KERNEL:  # the statistics kernel under one name, whatever its template arguments
-            return KERNEL
         return m.group(1) + (m.group(2) or "")
     if CALIBRATION_KERNEL in name:
         return CALIBRATION_KERNEL
@@ -80,6 +78,19 @@ def trace_stats(trace_dir):
                 rows.append((k, int(r["Calls"]), float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
                              float(r["MaxNs"]) / 1e3))
     return rows
+
+
+def is_stats(k):
+    """The bf16 statistics kernel, in either form (with or without the draft
+    entropy accumulator)."""
+    return k == KERNEL or k.startswith(KERNEL + "<")
+
+
+def stats_key(d):
+    """The statistics kernel's name among the keys of d (the form with the most
+    dispatches when both ran)."""
+    keys = [k for k in d if is_stats(k)]
+    return max(keys, key=lambda k: len(d[k])) if keys else None
 
 
 def median(v):
@@ -131,10 +142,11 @@ def main():
                 v = vals[n].get(k)
                 cells.append(f"{sum(v) / len(v):,.1f}" if v else "")
             lines.append(f"| {k} | " + " | ".join(cells) + " |")
-        if a.elements and "SQ_INSTS_VALU" in vals and KERNEL in vals["SQ_INSTS_VALU"]:
-            v = vals["SQ_INSTS_VALU"][KERNEL]
+        sk = stats_key(vals["SQ_INSTS_VALU"]) if "SQ_INSTS_VALU" in vals else None
+        if a.elements and sk:
+            v = vals["SQ_INSTS_VALU"][sk]
             per = sum(v) / len(v) / a.elements * 64
-            lines += ["", f"{KERNEL}: {a.elements:,.0f} element pairs per launch, {per:.1f} VALU wave "
+            lines += ["", f"{sk}: {a.elements:,.0f} element pairs per launch, {per:.1f} VALU wave "
                       "instructions per 64 element pairs."]
     if not (a.fetch and a.write):
         if bench and "loop" in bench:
@@ -152,9 +164,10 @@ def main():
     write = counter_values(a.write, "WRITE_SIZE")
     f_cal = median(fetch[CALIBRATION_KERNEL]) * 1024 / CALIBRATION_BYTES
     w_cal = median(write[CALIBRATION_KERNEL]) * 1024 / CALIBRATION_BYTES
-    f_k = median(fetch[KERNEL]) * 1024 / f_cal
-    w_k = median(write[KERNEL]) * 1024 / w_cal
-    traffic = {"workload": a.workload, "kernel": KERNEL, "kernel_source_hash": kernel_source_hash(),
+    sk = stats_key(fetch)
+    f_k = median(fetch[sk]) * 1024 / f_cal
+    w_k = median(write[sk]) * 1024 / w_cal
+    traffic = {"workload": a.workload, "kernel": sk, "kernel_source_hash": kernel_source_hash(),
                "fetch_bytes_per_launch": f_k, "write_bytes_per_launch": w_k, "bytes_per_launch": f_k + w_k,
                "fetch_counter_scale": 1.0 / f_cal, "write_counter_scale": 1.0 / w_cal,
                "algorithmic_bytes": a.algorithmic_bytes}
@@ -185,16 +198,16 @@ def main():
     if bench:
         r = bench
         ev_us = r["roofline"]["kernel_ms"] * 1e3
-        tr_us = [avg for k, _, avg, _, _ in trace_stats(a.trace) if k == KERNEL][0]
+        tr_us = [avg for k, _, avg, _, _ in trace_stats(a.trace) if k == sk][0]
         lines += ["", "## HIP events against the trace", "",
-                  f"bench.py run without the profiler on the same box: {KERNEL} timed with HIP events "
+                  f"bench.py run without the profiler on the same box: {sk} timed with HIP events "
                   f"{ev_us:.2f} us per launch over {r['steps']} steps (the roofline's `achieved` "
                   f"{r['roofline']['achieved']:.0f} GB/s); the trace above: {tr_us:.2f} us "
                   f"({(ev_us / tr_us - 1) * 100:+.1f}%). Step: {r['ms_per_step'] * 1e3:.2f} us, "
                   f"{r['value'] / 1e6:.2f} M rows/s. Under rocprofv3 each attached completion event "
                   "opens a gap of about 4.6 us before the next kernel, so the figure bench.py prints inside the "
                   "profiled process includes that gap."]
-    lines += ["", f"{KERNEL}: {traffic['bytes_per_launch'] / 1e6:.2f} MB per launch measured against "
+    lines += ["", f"{sk}: {traffic['bytes_per_launch'] / 1e6:.2f} MB per launch measured against "
               f"{a.algorithmic_bytes / 1e6:.2f} MB algorithmic "
               f"({traffic['bytes_per_launch'] / a.algorithmic_bytes:.4f}x).", ""]
     if bench and a.step_algorithmic_bytes:

@@ -200,6 +200,30 @@ def test_deterministic(gpu_lib, name):
         assert np.array_equal(a[k].view(np.uint32), b[k].view(np.uint32)), k
 
 
+@pytest.mark.parametrize("name", ["b64", "lowacc", "b256g"])
+def test_entropy_request_changes_nothing_else(gpu_lib, name):
+    """A call that asks for no draft entropy runs the statistics kernel without
+    the entropy accumulator; every other output is the same bit for bit as in
+    a call that asks for it."""
+    import torch
+    step = W.make_step(W.CONFIGS[name], seed=14, device="cuda")
+    announce(f"entropy request {name} B={step.B} N={step.N}")
+    runs = []
+    for ent in (True, False):
+        lse = torch.empty((max(step.N, 1), 2), dtype=torch.float64, device="cuda")[:step.N]
+        out = gpu_lib.verify(step.target, step.draft, step.sl, step.cu_sl, step.draft_tokens, step.temperature,
+                             step.u_acc, step.u_res, step.k_max, row_lse=lse, draft_entropy=ent)
+        torch.cuda.synchronize()
+        res = {k: v.cpu().numpy() for k, v in out.items()}
+        res["row_lse"] = lse.cpu().numpy()
+        runs.append(res)
+    a, b = runs
+    assert "draft_entropy" in a and "draft_entropy" not in b
+    for k in ("accepted", "tokens", "seq_err", "row_lse"):
+        assert np.array_equal(a[k], b[k]), k
+    assert np.array_equal(a["kld"].view(np.uint32), b["kld"].view(np.uint32))
+
+
 @pytest.mark.parametrize("name", ["b64", "b256", "lowacc", "b256g"])
 def test_fused_step_deterministic(gpu_lib, name):
     """dsde_step twice from the same controller state: every output and the
