@@ -123,7 +123,9 @@ size_t dsde_verify_workspace_bytes(int32_t B, int64_t N, int64_t V, int32_t k_ma
  *                                       log sum_v exp(z_v / T_b) of the target and draft rows
  *   draft_entropy [N]       float       optional (may be NULL): H(q) = -sum_v q_v ln q_v of
  *                                       each drafted position's draft distribution (nats),
- *                                       the draft-entropy signal of Sec. 4.2 / Table 2
+ *                                       the draft-entropy signal of Sec. 4.2 / Table 2;
+ *                                       NULL also skips its accumulation in the statistics
+ *                                       pass (every other output is unchanged, bit for bit)
  * The draw walks token ids in ascending order and returns the smallest id whose
  * cumulative weight exceeds u_res[b] times the total weight.  Acceptance is
  * evaluated as u < p(x)/q(x) in double precision.
